@@ -1,0 +1,315 @@
+"""fp64 CPU oracle for the acceptance-aware draft-training losses.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this module: only ``tests/``, ``__graft_entry__.smoke()`` and the CPU
+baseline leg of ``bench.py`` use it.  It shares no code with the HIP library.
+
+Every function is a plain, slow, literal transcription of a definition in
+"Acceptance-Aware Draft Model Training for Speculative Decoding"
+(arXiv 2609.24150), computed in float64 on the exact input values (bf16 and
+fp32 inputs are exactly representable in float64).  Array layout follows the
+library's: logits are ``[N, K, V]`` (N windows, K = the speculative window size
+gamma, V = vocabulary), row ``n*K + k`` is position ``k`` of window ``n``.
+
+Readings of places where the paper is silent (each is listed in the design doc):
+
+* temperature: Eq. (1) scales log-probabilities; ``tempered_log_softmax``
+  applies it literally to ``log softmax(z)``;
+* greedy token ``x*``: argmax of the raw target logits, lowest index on ties;
+* ``d min(p, q) / d q`` is taken as ``1[q < p]`` (0 at ties);
+* the loss is normalised by the number of windows (the window-start set W);
+* the simulated-acceptance draft token is the inverse-CDF sample of q with a
+  uniform ``u1`` (smallest v whose cumulative mass exceeds u1), accepted iff
+  ``u2 * q(x) < p(x)``; the group standard deviation uses ``ddof`` (default 0).
+
+Pinning: every function here is checked by ``tests/test_oracle_pins.py``
+against hand-computed cases, closed forms, identities the paper states,
+finite differences and brute-force enumeration.  No function is "parity
+unpinned".
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "tempered_log_softmax",
+    "greedy_token",
+    "acceptance_greedy",
+    "acceptance_sampling",
+    "total_variation",
+    "prob_accepted_at_least",
+    "length_distribution",
+    "expected_length_full",
+    "expected_length",
+    "expected_length_grad",
+    "eal_loss",
+    "wtv_loss",
+    "inverse_cdf_token",
+    "simulate_acceptance",
+    "group_advantage",
+    "sim_accept_grpo",
+    "sim_near_threshold",
+    "wtv_near_ties",
+]
+
+
+# ---------------------------------------------------------------------------
+# Temperature scaling (Section "Preliminaries and Notation", Eq. 1)
+# ---------------------------------------------------------------------------
+def _log_softmax(x: np.ndarray) -> np.ndarray:
+    """Log of a normalised exponential over the last axis, max-shifted."""
+    m = np.max(x, axis=-1, keepdims=True)
+    return x - (m + np.log(np.sum(np.exp(x - m), axis=-1, keepdims=True)))
+
+
+def tempered_log_softmax(z, T: float) -> np.ndarray:
+    """log p~ for logits z at temperature T > 0 (Eq. 1).
+
+    The paper defines p~(v) proportional to exp(log p(v) / T) with p the
+    untempered next-token distribution.  We first form log p = log softmax(z)
+    and then renormalise exp(log p / T), exactly in that order.
+    """
+    if not T > 0:
+        raise ValueError("temperature must be > 0")
+    logp = _log_softmax(np.asarray(z, dtype=np.float64))
+    return _log_softmax(logp / np.float64(T))
+
+
+# ---------------------------------------------------------------------------
+# Per-position acceptance (Eqs. acc_greedy and acc_sample)
+# ---------------------------------------------------------------------------
+def greedy_token(z_target) -> np.ndarray:
+    """x* = argmax_v p(v) = argmax_v z_t(v); lowest index on ties (Eq. acc_greedy)."""
+    return np.argmax(np.asarray(z_target, dtype=np.float64), axis=-1)
+
+
+def acceptance_greedy(z_draft, z_target, T_draft: float = 1.0):
+    """a = q(x*), the draft mass on the target's greedy token (Eq. acc_greedy).
+
+    Returns (a, x*, q).
+    """
+    q = np.exp(tempered_log_softmax(z_draft, T_draft))
+    xs = greedy_token(z_target)
+    a = np.take_along_axis(q, xs[..., None], axis=-1)[..., 0]
+    return a, xs, q
+
+
+def acceptance_sampling(z_draft, z_target, T_draft: float, T_target: float):
+    """a = sum_v min(p~(v), q~(v)) = 1 - TV (Eq. acc_sample, Eq. rejection_rate).
+
+    Returns (a, q, p).
+    """
+    q = np.exp(tempered_log_softmax(z_draft, T_draft))
+    p = np.exp(tempered_log_softmax(z_target, T_target))
+    a = np.sum(np.minimum(p, q), axis=-1)
+    return a, q, p
+
+
+def total_variation(p, q) -> np.ndarray:
+    """TV(p, q) = 1/2 sum_v |p(v) - q(v)| (used by Eq. rejection_rate)."""
+    return 0.5 * np.sum(np.abs(np.asarray(p, np.float64) - np.asarray(q, np.float64)), axis=-1)
+
+
+# ---------------------------------------------------------------------------
+# Speculative window (Eqs. eal_generic, eal_full, eal_compact)
+# ---------------------------------------------------------------------------
+def prob_accepted_at_least(a) -> np.ndarray:
+    """P(L >= k) = prod_{j<k} a_j for k = 1..K (Eq. eal_generic); shape [..., K]."""
+    return np.cumprod(np.asarray(a, np.float64), axis=-1)
+
+
+def length_distribution(a) -> np.ndarray:
+    """P(L = l) for l = 0..K from the three cases of Section "Expected Accepted
+    Length Loss": 1 - a_0, (prod_{j<l} a_j)(1 - a_l), and prod_{j<K} a_j.
+    Shape [..., K+1]."""
+    a = np.asarray(a, np.float64)
+    K = a.shape[-1]
+    out = np.empty(a.shape[:-1] + (K + 1,), np.float64)
+    out[..., 0] = 1.0 - a[..., 0]
+    for l in range(1, K):
+        out[..., l] = np.prod(a[..., :l], axis=-1) * (1.0 - a[..., l])
+    out[..., K] = np.prod(a, axis=-1)
+    return out
+
+
+def expected_length_full(a) -> np.ndarray:
+    """E[L] = sum_l l * P(L = l) (Eq. eal_full)."""
+    d = length_distribution(a)
+    ell = np.arange(d.shape[-1], dtype=np.float64)
+    return np.sum(ell * d, axis=-1)
+
+
+def expected_length(a) -> np.ndarray:
+    """E[L] = sum_{k=1..K} prod_{j<k} a_j (Eq. eal_compact / eal_generic)."""
+    return np.sum(prob_accepted_at_least(a), axis=-1)
+
+
+def expected_length_grad(a) -> np.ndarray:
+    """dE[L]/da_j, from the definition of Eq. eal_compact term by term.
+
+    E = sum_{k=1..K} prod_{i<k} a_i, so a_j appears in every term with k > j
+    and d(term_k)/da_j = prod_{i<k, i != j} a_i.  Computed without division,
+    so it is exact when some a_i is zero.
+    """
+    a = np.asarray(a, np.float64)
+    K = a.shape[-1]
+    g = np.zeros_like(a)
+    for j in range(K):
+        b = a.copy()
+        b[..., j] = 1.0
+        cp = np.cumprod(b, axis=-1)  # cp[k-1] = prod_{i<k, i != j} a_i
+        g[..., j] = np.sum(cp[..., j:], axis=-1)
+    return g
+
+
+# ---------------------------------------------------------------------------
+# Losses (Eq. loss_eal, Eq. loss_tv) and their gradients w.r.t. draft logits
+# ---------------------------------------------------------------------------
+def _window_loss(a):
+    """loss = -(1/|W|) sum_windows E[L]; g = dloss/da.  a has shape [N, K]."""
+    N = a.shape[0]
+    E = expected_length(a)
+    loss = -np.sum(E) / N
+    g = -expected_length_grad(a) / N
+    return loss, E, g
+
+
+def eal_loss(z_draft, z_target, T_draft: float = 1.0, grad_scale: float = 1.0):
+    """Greedy Expected-Accepted-Length loss and d loss / d z_draft (Eq. loss_eal).
+
+    a_{n,j} = q_{n,j}(x*_{n,j}) with q = softmax of the draft logits at T_draft.
+    The gradient chains dloss/da_j through the softmax Jacobian at temperature T:
+    d q(x*) / d z(v) = (1/T) q(x*) (1[v = x*] - q(v)).  The target is frozen.
+    ``grad_scale`` multiplies the returned gradient only (an upstream dL/dloss).
+
+    Returns a dict with loss, E [N], a [N,K], xstar [N,K], grad [N,K,V].
+    """
+    zd = np.asarray(z_draft, np.float64)
+    a, xs, q = acceptance_greedy(zd, z_target, T_draft)
+    loss, E, g = _window_loss(a)
+    onehot = np.zeros_like(q)
+    np.put_along_axis(onehot, xs[..., None], 1.0, axis=-1)
+    grad = (grad_scale * g * a / T_draft)[..., None] * (onehot - q)
+    return {"loss": loss, "E": E, "a": a, "xstar": xs, "grad": grad}
+
+
+def wtv_loss(z_draft, z_target, T_draft: float, T_target: float, grad_scale: float = 1.0):
+    """Window-TV loss and d loss / d z_draft (Eq. loss_tv).
+
+    a_{n,j} = sum_v min(p(v), q(v)) = 1 - TV.  With the reading
+    d min(p, q)/dq = 1[q < p], d a / d q(u) = m(u) = 1[q(u) < p(u)], and the
+    softmax Jacobian gives d a / d z(v) = (1/T_d) q(v) (m(v) - sum_u m(u) q(u)).
+    Gradients flow only into the draft (the target is frozen).
+
+    Returns a dict with loss, E [N], a [N,K], qlt [N,K] (= sum of q where
+    q < p), tv [N,K], grad [N,K,V].
+    """
+    a, q, p = acceptance_sampling(z_draft, z_target, T_draft, T_target)
+    loss, E, g = _window_loss(a)
+    m = (q < p).astype(np.float64)
+    qlt = np.sum(m * q, axis=-1)
+    grad = (grad_scale * g / T_draft)[..., None] * q * (m - qlt[..., None])
+    return {"loss": loss, "E": E, "a": a, "qlt": qlt, "tv": total_variation(p, q), "grad": grad}
+
+
+# ---------------------------------------------------------------------------
+# Simulated acceptance length and group-relative advantage (Section "GRPO Loss
+# on Acceptance Length"; sampling verification of Eq. acc_sample)
+# ---------------------------------------------------------------------------
+def inverse_cdf_token(q, u1) -> np.ndarray:
+    """Draft token drawn from q with the uniform u1: the smallest v with
+    sum_{w <= v} q(w) > u1.  If rounding leaves no such v, the last v with
+    q(v) > 0 is taken."""
+    q = np.asarray(q, np.float64)
+    C = np.cumsum(q, axis=-1)
+    x = np.sum(C <= np.asarray(u1, np.float64)[..., None], axis=-1)
+    V = q.shape[-1]
+    over = x >= V
+    if np.any(over):
+        last_pos = V - 1 - np.argmax((q > 0)[..., ::-1], axis=-1)
+        x = np.where(over, last_pos, x)
+    return x
+
+
+def simulate_acceptance(z_draft, z_target, T: float, u1, u2):
+    """One simulated sampling-verification pass over windows of K positions.
+
+    Per position: draw x ~ q~ by inverse CDF with u1, accept iff u2 < min(1, p~(x)/q~(x))
+    (evaluated as u2 * q~(x) < p~(x)); the reward is the accepted length
+    sum_k prod_{j<=k} accept_j, i.e. the count up to the first rejection
+    (Section "Reward construction via simulated greedy verification", in its
+    sampling-verification form).
+
+    z_* have shape [..., K, V]; u1, u2 have shape [..., K].
+    Returns (token, accept, reward, q, p).
+    """
+    q = np.exp(tempered_log_softmax(z_draft, T))
+    p = np.exp(tempered_log_softmax(z_target, T))
+    x = inverse_cdf_token(q, u1)
+    qx = np.take_along_axis(q, x[..., None], axis=-1)[..., 0]
+    px = np.take_along_axis(p, x[..., None], axis=-1)[..., 0]
+    acc = np.asarray(u2, np.float64) * qx < px
+    reward = np.sum(np.cumprod(acc.astype(np.int64), axis=-1), axis=-1)
+    return x, acc, reward, q, p
+
+
+def group_advantage(reward, eps: float = 1e-6, ddof: int = 0, clip: float | None = None):
+    """A = clip((R - mean_g R) / (std_g R + eps), -C_A, C_A) (Eq. advantage).
+
+    ``reward`` has shape [P, G]: P groups of G samples.  std is the group
+    standard deviation with ``ddof`` (0: population).  ``clip`` None or <= 0
+    leaves A unclipped.
+    """
+    r = np.asarray(reward, np.float64)
+    G = r.shape[-1]
+    mean = np.sum(r, axis=-1, keepdims=True) / G
+    std = np.sqrt(np.sum((r - mean) ** 2, axis=-1, keepdims=True) / (G - ddof))
+    A = (r - mean) / (std + eps)
+    if clip is not None and clip > 0:
+        A = np.clip(A, -clip, clip)
+    return A
+
+
+def sim_accept_grpo(z_draft, z_target, T: float, u1, u2, eps: float = 1e-6,
+                    ddof: int = 0, clip: float | None = None):
+    """Simulated acceptance reward and group advantages.
+
+    z_* have shape [P, G, K, V], u1 and u2 [P, G, K].
+    Returns a dict with token [P,G,K], accept [P,G,K], reward [P,G], advantage [P,G].
+    """
+    x, acc, r, _, _ = simulate_acceptance(z_draft, z_target, T, u1, u2)
+    return {"token": x, "accept": acc, "reward": r,
+            "advantage": group_advantage(r, eps, ddof, clip)}
+
+
+# ---------------------------------------------------------------------------
+# Flags for decisions that sit on a floating-point boundary
+# ---------------------------------------------------------------------------
+def sim_near_threshold(z_draft, z_target, T: float, u1, u2, tol: float = 1e-6):
+    """Per position: True where u1 lies within ``tol`` of a CDF boundary of the
+    chosen token, or u2 within ``tol`` of min(1, p/q) at that token.  Such
+    decisions may legitimately differ between fp64 and a lower precision."""
+    q = np.exp(tempered_log_softmax(z_draft, T))
+    p = np.exp(tempered_log_softmax(z_target, T))
+    u1 = np.asarray(u1, np.float64)
+    x = inverse_cdf_token(q, u1)
+    C = np.cumsum(q, axis=-1)
+    hi = np.take_along_axis(C, x[..., None], axis=-1)[..., 0]
+    lo = hi - np.take_along_axis(q, x[..., None], axis=-1)[..., 0]
+    near1 = (np.abs(u1 - lo) <= tol) | (np.abs(u1 - hi) <= tol)
+    qx = np.take_along_axis(q, x[..., None], axis=-1)[..., 0]
+    px = np.take_along_axis(p, x[..., None], axis=-1)[..., 0]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        thr = np.minimum(1.0, np.where(qx > 0, px / qx, 1.0))
+    near2 = np.abs(np.asarray(u2, np.float64) - thr) <= tol
+    return near1 | near2
+
+
+def wtv_near_ties(z_draft, z_target, T_draft: float, T_target: float, rel: float = 1e-5):
+    """Per row: the largest q(v) among entries whose q and p agree to ``rel``
+    relative.  At such entries 1[q < p] may flip between precisions; the
+    gradient of the row then moves by at most |coef| * q(v) * (1 + max q)."""
+    q = np.exp(tempered_log_softmax(z_draft, T_draft))
+    p = np.exp(tempered_log_softmax(z_target, T_target))
+    near = np.abs(q - p) <= rel * np.maximum(p, q)
+    return np.max(np.where(near, q, 0.0), axis=-1)
