@@ -1,0 +1,239 @@
+"""Benchmark: fused WTV loss forward + backward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2]
+
+A step is one aal_wtv_fwd_bwd call (per-row softmaxes of both logit sets,
+sum min(p, q), window prefix products, loss, and dloss/dz_draft) over the
+whole workload, inputs resident in HBM.  The default workload is the WTV
+configuration at V=128256 bf16: N=2048 windows x K=7 positions, T=1.0 for
+both distributions, bf16 gradient.
+
+Prints ONE JSON line.  `value` is logit rows/s; `roofline` prices the step
+against HBM bandwidth with the algorithmic byte count (both logit tensors read
+once, the gradient written once: (2 s_in + s_grad) V bytes per row) over the
+average step time measured with HIP events on the stream the kernels run on.
+Secondary measurements (EAL on the same inputs, the simulated-acceptance
+reward on the GRPO workload) are reported under "also".  `cpu_baseline` times
+the fp64 oracle on a bounded sample of the same workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import multiprocessing as mp
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+WORKLOAD_TEXT = {
+    "c2": "WTV fwd+bwd: N=2048 windows x K=7 x V=128256, bf16 logits, bf16 grad, T=1.0/1.0",
+    "c4": "WTV fwd+bwd: N=16384 windows x K=16 x V=32000, fp32 logits, fp32 grad, T=0.5/0.5",
+}
+
+
+# ------------------------------------------------------------- CPU baseline
+def _cpu_worker(args):
+    wid, recipe, K, V, nwin, budget_s = args
+    import numpy as np
+    import torch
+
+    import oracle as O
+    from paper_2609_24150_amd.inputs import CONFIGS, make_logits
+    cfg = CONFIGS[recipe]
+    torch.set_num_threads(1)
+    zd, zt = make_logits(cfg["recipe"], (nwin, K, V), cfg["dtype"], seed=1000 + wid, device="cpu")
+    zd = zd.to(torch.float64).numpy()
+    zt = zt.to(torch.float64).numpy()
+    Td, Tt = cfg["temp_draft"], cfg["temp_target"]
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        O.wtv_loss(zd, zt, Td, Tt)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            return n * nwin * K, el
+
+
+def cpu_baseline(workload: str, budget_s: float = 12.0) -> dict:
+    from paper_2609_24150_amd.inputs import CONFIGS
+    cfg = CONFIGS[workload]
+    K, V = cfg["K"], cfg["V"]
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    workers = max(1, min(16, cores))
+    nwin = 2
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(workers) as pool:
+        res = pool.map(_cpu_worker, [(w, workload, K, V, nwin, budget_s) for w in range(workers)])
+    wall = time.perf_counter() - t0
+    rows = sum(r[0] for r in res)
+    # each worker's rate over its own timed loop, summed: the aggregate rate
+    rate = sum(r[0] / r[1] for r in res)
+    return {"value": rate, "unit": "logit rows/s", "cores": workers, "kind": "oracle",
+            "sample": f"{workers} processes x {nwin} windows of the workload (K={K}, V={V}), each repeated "
+                      f"for ~{budget_s:.0f}s; {rows} rows in {wall:.1f}s wall"}
+
+
+# ----------------------------------------------------------------- GPU legs
+def _time_calls(fn, steps, warmup, stream):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        fn()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) / steps  # ms per call
+
+
+def loss_call(op, inp, grad_dtype, flags=0):
+    """A zero-allocation closure over the C entry point with preallocated outputs."""
+    import torch
+
+    import paper_2609_24150_amd as A
+    from paper_2609_24150_amd import _lib
+    zd, zt = inp["z_draft"], inp["z_target"]
+    cfg = inp["cfg"]
+    N, K, V = zd.shape
+    dev = zd.device
+    loss = torch.empty(1, device=dev)
+    E = torch.empty(N, device=dev)
+    acc = torch.empty(N, K, device=dev)
+    grad = torch.empty(N, K, V, dtype=grad_dtype, device=dev)
+    ws = A.workspace(N * K, N, dev)
+    L = _lib.lib()
+    stream = torch.cuda.current_stream(dev)
+    dcode = _lib.AAL_BF16 if zd.dtype == torch.bfloat16 else _lib.AAL_F32
+    gcode = _lib.AAL_BF16 if grad_dtype == torch.bfloat16 else _lib.AAL_F32
+    if op == "wtv":
+        Td, Tt = cfg.get("temp_draft", 1.0), cfg.get("temp_target", cfg.get("wtv_temp", 1.0))
+
+        def fn():
+            st = L.aal_wtv_fwd_bwd(zd.data_ptr(), zt.data_ptr(), dcode, N, K, V, Td, Tt, loss.data_ptr(),
+                                   E.data_ptr(), acc.data_ptr(), grad.data_ptr(), gcode, None, flags,
+                                   ws.data_ptr(), ws.numel(), stream.cuda_stream)
+            _lib.check(st, "aal_wtv_fwd_bwd")
+    else:
+        xs = torch.empty(N, K, dtype=torch.int32, device=dev)
+        Td = cfg.get("temp_draft", 1.0)
+
+        def fn():
+            st = L.aal_eal_fwd_bwd(zd.data_ptr(), zt.data_ptr(), dcode, N, K, V, Td, loss.data_ptr(),
+                                   E.data_ptr(), acc.data_ptr(), xs.data_ptr(), grad.data_ptr(), gcode, None,
+                                   flags, ws.data_ptr(), ws.numel(), stream.cuda_stream)
+            _lib.check(st, "aal_eal_fwd_bwd")
+    return fn, stream, {"loss": loss, "E": E, "grad": grad}
+
+
+def sim_call(inp):
+    import torch
+
+    import paper_2609_24150_amd as A
+    from paper_2609_24150_amd import _lib
+    zd, zt, u1, u2 = inp["z_draft"], inp["z_target"], inp["u1"], inp["u2"]
+    P, G, K, V = zd.shape
+    dev = zd.device
+    tok = torch.empty(P, G, K, dtype=torch.int32, device=dev)
+    acc = torch.empty_like(tok)
+    rew = torch.empty(P, G, dtype=torch.int32, device=dev)
+    adv = torch.empty(P, G, device=dev)
+    ws = A.workspace(P * G * K, P * G, dev)
+    L = _lib.lib()
+    stream = torch.cuda.current_stream(dev)
+    dcode = _lib.AAL_BF16 if zd.dtype == torch.bfloat16 else _lib.AAL_F32
+
+    def fn():
+        st = L.aal_sim_accept_grpo(zd.data_ptr(), zt.data_ptr(), dcode, P, G, K, V, 1.0, u1.data_ptr(),
+                                   u2.data_ptr(), tok.data_ptr(), acc.data_ptr(), rew.data_ptr(), adv.data_ptr(),
+                                   1e-6, 0, 0.0, ws.data_ptr(), ws.numel(), stream.cuda_stream)
+        _lib.check(st, "aal_sim_accept_grpo")
+    return fn, stream
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-also", action="store_true", help="skip the secondary EAL and simulation legs")
+    ap.add_argument("--flags", type=int, default=0, help="AAL_FLAG_* bits for the timed call")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    # The CPU leg runs first, in forked workers, before this process touches the GPU.
+    cpu = None if args.no_cpu_baseline else cpu_baseline(args.workload)
+
+    import torch
+
+    from paper_2609_24150_amd.inputs import CONFIGS, make_config
+    cfg = CONFIGS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    inp = make_config(args.workload, seed=0, device=dev)
+    N, K, V = cfg["N"], cfg["K"], cfg["V"]
+    rows = N * K
+    s_in = 2 if cfg["dtype"] == torch.bfloat16 else 4
+    gdt = cfg["dtype"]
+    s_g = s_in
+    fn, stream, _ = loss_call("wtv", inp, gdt, args.flags)
+    ms = _time_calls(fn, args.steps, args.warmup, stream)
+    alg_bytes = rows * (2 * s_in + s_g) * V
+    achieved = alg_bytes / (ms * 1e-3) / 1e9
+    out = {
+        "metric": "EAL/WTV fwd+bwd logit rows/s + % of HBM peak, V=128256 bf16, 1 GPU",
+        "value": rows / (ms * 1e-3),
+        "unit": "logit rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg["dtype"] == torch.bfloat16 else "f32",
+        "data": "synthetic (seeded logits with the workload's distribution)",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "N": N, "K": K, "V": V,
+                   "windows_per_s": N / (ms * 1e-3)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "bytes_per_step": alg_bytes, "kernel": "whole aal_wtv_fwd_bwd call"},
+        "cpu_baseline": cpu,
+    }
+    if not args.no_also:
+        also = {}
+        fn_e, st_e, _ = loss_call("eal", inp, gdt, args.flags)
+        ms_e = _time_calls(fn_e, args.steps, args.warmup, st_e)
+        also["eal_same_inputs"] = {"ms": ms_e, "rows_per_s": rows / (ms_e * 1e-3),
+                                   "alg_GBps": rows * (2 * s_in + s_g) * V / (ms_e * 1e-3) / 1e9}
+        del inp
+        torch.cuda.empty_cache()
+        sim = make_config("c5", seed=0, device=dev)
+        c5 = CONFIGS["c5"]
+        rows5 = c5["P"] * c5["G"] * c5["K"]
+        fn_s, st_s = sim_call(sim)
+        ms_s = _time_calls(fn_s, args.steps, args.warmup, st_s)
+        also["sim_grpo_c5"] = {"ms": ms_s, "rows_per_s": rows5 / (ms_s * 1e-3),
+                               "alg_GBps": rows5 * 2 * 2 * c5["V"] / (ms_s * 1e-3) / 1e9}
+        out["also"] = also
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

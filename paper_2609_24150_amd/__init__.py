@@ -1,0 +1,17 @@
+"""Acceptance-aware draft-training losses (EAL, WTV) and the simulated
+acceptance-length GRPO reward on AMD Instinct MI355X (gfx950).
+
+The computation runs in hand-written HIP kernels inside libaal.so (C ABI in
+include/aal.h); this package only marshals torch tensors to it.
+"""
+from .api import (  # noqa: F401
+    AAL_BF16,
+    AAL_F32,
+    AAL_FLAG_STREAMING,
+    aal_eal_fwd_bwd,
+    aal_sim_accept_grpo,
+    aal_workspace_bytes,
+    aal_wtv_fwd_bwd,
+    workspace,
+)
+from ._lib import AalError, LIB_PATH  # noqa: F401

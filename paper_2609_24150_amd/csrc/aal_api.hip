@@ -1,0 +1,244 @@
+// C ABI of libaal: argument validation, workspace carve-up and dispatch.
+// Declarations and the contract of every entry point are in include/aal.h.
+#include "aal.h"
+#include "aal_internal.h"
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+namespace {
+
+thread_local std::string g_last_error;
+
+aal_status_t fail(aal_status_t s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+// Finite and > 0, checked on the bit pattern so that no floating-point
+// compilation mode can fold the test away.
+bool positive_finite(float x) {
+  uint32_t u;
+  memcpy(&u, &x, sizeof u);
+  const bool sign = (u >> 31) != 0;
+  const uint32_t expo = (u >> 23) & 0xffu;
+  return !sign && expo != 0xffu && (u & 0x7fffffffu) != 0;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+bool valid_dtype(int d) { return d == AAL_BF16 || d == AAL_F32; }
+
+aal::DType to_dtype(int d) { return d == AAL_BF16 ? aal::DType::kBf16 : aal::DType::kF32; }
+
+constexpr double kLog2e = 1.4426950408889634073599246810019;
+
+// log2(e)/T as a finite positive float, or 0 if it is not representable.
+float scale_for(float T) {
+  const double s = kLog2e / double(T);
+  if (!(s < 3.0e38)) return 0.f;
+  const float f = float(s);
+  return positive_finite(f) ? f : 0.f;
+}
+
+struct CommonIn {
+  const void* zd;
+  const void* zt;
+  int in_dtype;
+  int64_t N;
+  int32_t K;
+  int32_t V;
+  float* loss;
+  void* grad;
+  int grad_dtype;
+  void* workspace;
+  size_t workspace_bytes;
+};
+
+aal_status_t validate_common(const CommonIn& c) {
+  if (!c.zd || !c.zt) return fail(AAL_ERR_ARG, "z_draft and z_target must be non-NULL");
+  if (!c.loss) return fail(AAL_ERR_ARG, "loss must be non-NULL");
+  if (c.N < 1) return fail(AAL_ERR_ARG, "N must be >= 1 (got %lld)", (long long)c.N);
+  if (c.K < 1 || c.K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", c.K);
+  if (c.V < 1) return fail(AAL_ERR_ARG, "V must be >= 1 (got %d)", c.V);
+  if (c.N > (int64_t(1) << 31) / c.K) return fail(AAL_ERR_ARG, "N*K must be < 2^31");
+  if (c.N * c.K > (int64_t(1) << 62) / c.V) return fail(AAL_ERR_ARG, "N*K*V must be < 2^62");
+  if (!valid_dtype(c.in_dtype)) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", c.in_dtype);
+  if (c.grad && !valid_dtype(c.grad_dtype)) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", c.grad_dtype);
+  if (!aligned(c.zd, 16) || !aligned(c.zt, 16)) return fail(AAL_ERR_ALIGN, "logit pointers must be 16-byte aligned");
+  if (c.grad && !aligned(c.grad, 16)) return fail(AAL_ERR_ALIGN, "grad_draft must be 16-byte aligned");
+  if (!c.workspace) return fail(AAL_ERR_WORKSPACE, "workspace must be non-NULL");
+  if (!aligned(c.workspace, 256)) return fail(AAL_ERR_ALIGN, "workspace must be 256-byte aligned");
+  const size_t need = aal::workspace_bytes(c.N * c.K, c.N);
+  if (c.workspace_bytes < need)
+    return fail(AAL_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", c.workspace_bytes, need);
+  return AAL_OK;
+}
+
+aal_status_t run_loss(aal::LossArgs& a) {
+  hipError_t e = aal::launch_streaming(a);
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int aal_version(void) { return 100; }
+
+size_t aal_workspace_bytes(int64_t rows, int64_t windows) {
+  if (rows < 0 || windows < 0) return 0;
+  return aal::workspace_bytes(rows, windows);
+}
+
+const char* aal_status_string(int status) {
+  switch (status) {
+    case AAL_OK: return "AAL_OK";
+    case AAL_ERR_ARG: return "AAL_ERR_ARG: invalid argument";
+    case AAL_ERR_DTYPE: return "AAL_ERR_DTYPE: unsupported element type";
+    case AAL_ERR_ALIGN: return "AAL_ERR_ALIGN: misaligned pointer";
+    case AAL_ERR_WORKSPACE: return "AAL_ERR_WORKSPACE: workspace missing or too small";
+    case AAL_ERR_HIP: return "AAL_ERR_HIP: HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* aal_last_error(void) { return g_last_error.c_str(); }
+
+aal_status_t aal_eal_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N, int32_t K,
+                             int32_t V, float temp_draft, float* loss, float* eal_per_window, float* accept,
+                             int32_t* target_argmax, void* grad_draft, aal_dtype_t grad_dtype,
+                             const float* grad_scale, uint32_t flags, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  g_last_error.clear();
+  const CommonIn c{z_draft, z_target, int(in_dtype), N, K, V, loss, grad_draft, int(grad_dtype),
+                   workspace, workspace_bytes};
+  aal_status_t s = validate_common(c);
+  if (s != AAL_OK) return s;
+  const float scd = scale_for(temp_draft);
+  if (!positive_finite(temp_draft) || scd == 0.f)
+    return fail(AAL_ERR_ARG, "temp_draft must be finite, > 0 and >= 1e-37");
+  if (flags & ~AAL_FLAG_STREAMING) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
+  aal::LossArgs a{};
+  a.mode = aal::Mode::kEal;
+  a.in = to_dtype(in_dtype);
+  a.gd = to_dtype(grad_dtype);
+  a.zd = z_draft;
+  a.zt = z_target;
+  a.N = N;
+  a.K = K;
+  a.V = V;
+  a.sc_d = scd;
+  a.sc_t = 0.f;
+  a.inv_t_d = 1.0f / temp_draft;
+  a.loss = loss;
+  a.ws = aal::carve(workspace, N * K, N);
+  a.window_e = eal_per_window ? eal_per_window : a.ws.window_e;
+  a.accept = accept;
+  a.xstar = target_argmax;
+  a.grad = grad_draft;
+  a.grad_scale = grad_scale;
+  a.stream = static_cast<hipStream_t>(stream);
+  return run_loss(a);
+}
+
+aal_status_t aal_wtv_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N, int32_t K,
+                             int32_t V, float temp_draft, float temp_target, float* loss, float* eal_per_window,
+                             float* accept, void* grad_draft, aal_dtype_t grad_dtype, const float* grad_scale,
+                             uint32_t flags, void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  const CommonIn c{z_draft, z_target, int(in_dtype), N, K, V, loss, grad_draft, int(grad_dtype),
+                   workspace, workspace_bytes};
+  aal_status_t s = validate_common(c);
+  if (s != AAL_OK) return s;
+  const float scd = scale_for(temp_draft);
+  const float sct = scale_for(temp_target);
+  if (!positive_finite(temp_draft) || scd == 0.f)
+    return fail(AAL_ERR_ARG, "temp_draft must be finite, > 0 and >= 1e-37");
+  if (!positive_finite(temp_target) || sct == 0.f)
+    return fail(AAL_ERR_ARG, "temp_target must be finite, > 0 and >= 1e-37");
+  if (flags & ~AAL_FLAG_STREAMING) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
+  aal::LossArgs a{};
+  a.mode = aal::Mode::kWtv;
+  a.in = to_dtype(in_dtype);
+  a.gd = to_dtype(grad_dtype);
+  a.zd = z_draft;
+  a.zt = z_target;
+  a.N = N;
+  a.K = K;
+  a.V = V;
+  a.sc_d = scd;
+  a.sc_t = sct;
+  a.inv_t_d = 1.0f / temp_draft;
+  a.loss = loss;
+  a.ws = aal::carve(workspace, N * K, N);
+  a.window_e = eal_per_window ? eal_per_window : a.ws.window_e;
+  a.accept = accept;
+  a.xstar = nullptr;
+  a.grad = grad_draft;
+  a.grad_scale = grad_scale;
+  a.stream = static_cast<hipStream_t>(stream);
+  return run_loss(a);
+}
+
+aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int32_t P,
+                                 int32_t G, int32_t K, int32_t V, float temperature, const float* u1,
+                                 const float* u2, int32_t* draft_token, int32_t* accept, int32_t* reward,
+                                 float* advantage, float eps, int32_t std_ddof, float adv_clip, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (!z_draft || !z_target || !u1 || !u2) return fail(AAL_ERR_ARG, "z_draft, z_target, u1, u2 must be non-NULL");
+  if (!reward || !advantage) return fail(AAL_ERR_ARG, "reward and advantage must be non-NULL");
+  if (P < 1 || G < 1 || K < 1 || V < 1) return fail(AAL_ERR_ARG, "P, G, K, V must be >= 1");
+  if (V > (1 << 21)) return fail(AAL_ERR_ARG, "V must be <= 2^21 (got %d)", V);
+  if (std_ddof < 0 || G <= std_ddof) return fail(AAL_ERR_ARG, "need 0 <= std_ddof < G");
+  const int64_t rows = int64_t(P) * G * K;
+  if (rows >= (int64_t(1) << 31)) return fail(AAL_ERR_ARG, "P*G*K must be < 2^31");
+  if (!valid_dtype(int(in_dtype))) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", int(in_dtype));
+  const float sc = scale_for(temperature);
+  if (!positive_finite(temperature) || sc == 0.f)
+    return fail(AAL_ERR_ARG, "temperature must be finite, > 0 and >= 1e-37");
+  uint32_t eb;
+  memcpy(&eb, &eps, sizeof eb);
+  if ((eb >> 31) || ((eb >> 23) & 0xffu) == 0xffu) return fail(AAL_ERR_ARG, "eps must be finite and >= 0");
+  if (!aligned(z_draft, 16) || !aligned(z_target, 16)) return fail(AAL_ERR_ALIGN, "logit pointers must be 16-byte aligned");
+  if (!workspace) return fail(AAL_ERR_WORKSPACE, "workspace must be non-NULL");
+  if (!aligned(workspace, 256)) return fail(AAL_ERR_ALIGN, "workspace must be 256-byte aligned");
+  const size_t need = aal::workspace_bytes(rows, int64_t(P) * G);
+  if (workspace_bytes < need) return fail(AAL_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+  aal::Workspace ws = aal::carve(workspace, rows, int64_t(P) * G);
+  int32_t* scratch = reinterpret_cast<int32_t*>(ws.stats);  // rows * 32 bytes >= 2 int32 per row
+  aal::SimArgs a{};
+  a.in = to_dtype(in_dtype);
+  a.zd = z_draft;
+  a.zt = z_target;
+  a.P = P;
+  a.G = G;
+  a.K = K;
+  a.V = V;
+  a.sc = sc;
+  a.u1 = u1;
+  a.u2 = u2;
+  a.token = draft_token ? draft_token : scratch;
+  a.accept = accept ? accept : scratch + rows;
+  a.reward = reward;
+  a.advantage = advantage;
+  a.eps = eps;
+  a.ddof = std_ddof;
+  a.clip = adv_clip;
+  a.stream = static_cast<hipStream_t>(stream);
+  hipError_t e = aal::launch_sim(a);
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
+}  // extern "C"

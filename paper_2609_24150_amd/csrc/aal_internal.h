@@ -1,0 +1,104 @@
+// Host-side interfaces between the C-ABI layer and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace aal {
+
+enum class Mode : int { kEal = 0, kWtv = 1 };
+enum class DType : int { kBf16 = 0, kF32 = 1 };
+
+// Per-row statistics written by the row pass and read by the window scan and
+// the gradient pass.  32 bytes.
+//   msc_*: fl(max_v z_v * sc) with sc = log2(e)/T, the reference of the sums
+//   l2s_*: log2 of sum_v 2^(z_v*sc - msc)
+// so that log2 q(v) = (z_v*sc - msc) - l2s.
+struct RowStats {
+  float msc_d, l2s_d;
+  float msc_t, l2s_t;
+  float a;      // per-position acceptance
+  float qlt;    // WTV: sum of q over entries with q < p
+  float coef;   // gradient coefficient (window scan output)
+  int32_t xstar;  // EAL: greedy target token
+};
+static_assert(sizeof(RowStats) == 32, "RowStats layout");
+
+// Workspace carve-up (all offsets 256-byte aligned).
+struct Workspace {
+  RowStats* stats;   // rows
+  float* window_e;   // windows
+  uint8_t* resident; // fixed region for the resident schedule
+  size_t resident_bytes;
+};
+
+constexpr size_t kResidentRegionBytes = size_t(4) << 20;
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+inline size_t workspace_bytes(int64_t rows, int64_t windows) {
+  return align256(size_t(rows) * sizeof(RowStats)) + align256(size_t(windows) * sizeof(float)) +
+         kResidentRegionBytes;
+}
+
+inline Workspace carve(void* base, int64_t rows, int64_t windows) {
+  uint8_t* p = static_cast<uint8_t*>(base);
+  Workspace w;
+  w.stats = reinterpret_cast<RowStats*>(p);
+  p += align256(size_t(rows) * sizeof(RowStats));
+  w.window_e = reinterpret_cast<float*>(p);
+  p += align256(size_t(windows) * sizeof(float));
+  w.resident = p;
+  w.resident_bytes = kResidentRegionBytes;
+  return w;
+}
+
+// Arguments of one EAL/WTV call after validation.
+struct LossArgs {
+  Mode mode;
+  DType in;
+  DType gd;
+  const void* zd;
+  const void* zt;
+  int64_t N;
+  int K;
+  int V;
+  float sc_d;      // log2(e)/T_draft
+  float sc_t;      // log2(e)/T_target (WTV)
+  float inv_t_d;   // 1/T_draft
+  float* loss;
+  float* window_e;  // user array or workspace
+  float* accept;    // may be null
+  int32_t* xstar;   // may be null
+  void* grad;       // may be null
+  const float* grad_scale;  // may be null
+  Workspace ws;
+  hipStream_t stream;
+};
+
+// Multi-kernel streaming schedule: row pass, window scan, loss reduction,
+// gradient pass.  Handles every shape.
+hipError_t launch_streaming(const LossArgs& a);
+
+struct SimArgs {
+  DType in;
+  const void* zd;
+  const void* zt;
+  int P, G, K, V;
+  float sc;
+  const float* u1;
+  const float* u2;
+  int32_t* token;   // rows (user or workspace)
+  int32_t* accept;  // rows (user or workspace)
+  int32_t* reward;
+  float* advantage;
+  float eps;
+  int ddof;
+  float clip;
+  hipStream_t stream;
+};
+
+hipError_t launch_sim(const SimArgs& a);
+
+}  // namespace aal

@@ -1,0 +1,97 @@
+"""CPU checks of the C ABI: the library loads, exports every function that
+include/aal.h declares, and rejects invalid arguments before touching a GPU.
+No call here reaches a kernel launch."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "aal.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(aal_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2609_24150_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.fail("libaal.so is not built (run __graft_entry__.build())")
+    return _lib
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("aal_eal_fwd_bwd", "aal_wtv_fwd_bwd", "aal_sim_accept_grpo", "aal_workspace_bytes",
+              "aal_status_string", "aal_last_error", "aal_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    h = C.CDLL(lib.LIB_PATH)
+    for n in declared_functions():
+        assert hasattr(h, n), f"{n} not exported"
+    assert set(lib._SIGNATURES) == set(declared_functions())
+
+
+def test_status_strings_and_version(lib):
+    L = lib.lib()
+    assert L.aal_version() >= 100
+    for s in range(6):
+        assert L.aal_status_string(s).decode().startswith("AAL_")
+    assert L.aal_status_string(99) == b"unknown status"
+
+
+def test_workspace_bytes(lib):
+    L = lib.lib()
+    a = L.aal_workspace_bytes(14336, 2048)
+    b = L.aal_workspace_bytes(28672, 2048)
+    assert b > a > 0 and a % 256 == 0
+    assert L.aal_workspace_bytes(-1, 3) == 0
+
+
+def _eal(L, **kw):
+    args = dict(zd=16, zt=16, dt=0, N=2, K=3, V=8, T=1.0, loss=16, grad=None, gdt=0, ws=256, wsb=1 << 30)
+    args.update(kw)
+    return L.aal_eal_fwd_bwd(args["zd"], args["zt"], args["dt"], args["N"], args["K"], args["V"], args["T"],
+                             args["loss"], None, None, None, args["grad"], args["gdt"], None, 0, args["ws"],
+                             args["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(zd=None), 1), (dict(loss=None), 1), (dict(N=0), 1), (dict(K=0), 1), (dict(K=65), 1),
+    (dict(V=0), 1), (dict(T=0.0), 1), (dict(T=-1.0), 1), (dict(T=float("nan")), 1), (dict(T=float("inf")), 1),
+    (dict(T=1e-45), 1), (dict(dt=7), 2), (dict(grad=16, gdt=9), 2), (dict(zd=18), 3), (dict(grad=24), 3),
+    (dict(ws=None), 4), (dict(ws=128), 3), (dict(wsb=100), 4), (dict(N=1 << 30, K=4), 1),
+])
+def test_eal_validation(lib, kw, code):
+    L = lib.lib()
+    assert _eal(L, **kw) == code
+    assert L.aal_last_error().decode() != ""
+
+
+def test_wtv_and_sim_validation(lib):
+    L = lib.lib()
+    st = L.aal_wtv_fwd_bwd(16, 16, 0, 2, 3, 8, 1.0, 0.0, 16, None, None, None, 0, None, 0, 256, 1 << 30, None)
+    assert st == 1 and b"temp_target" in L.aal_last_error()
+    st = L.aal_wtv_fwd_bwd(16, 16, 0, 2, 3, 8, 1.0, 1.0, 16, None, None, None, 0, None, 4, 256, 1 << 30, None)
+    assert st == 1 and b"flags" in L.aal_last_error()
+
+    def sim(**kw):
+        a = dict(P=2, G=4, K=3, V=10, T=1.0, u1=16, rew=16, eps=1e-6, ddof=0, ws=256, wsb=1 << 30)
+        a.update(kw)
+        return L.aal_sim_accept_grpo(16, 16, 0, a["P"], a["G"], a["K"], a["V"], a["T"], a["u1"], 16, None, None,
+                                     a["rew"], 16, a["eps"], a["ddof"], 0.0, a["ws"], a["wsb"], None)
+    assert sim(u1=None) == 1
+    assert sim(rew=None) == 1
+    assert sim(G=1, ddof=1) == 1
+    assert sim(V=(1 << 21) + 1) == 1
+    assert sim(T=float("nan")) == 1
+    assert sim(eps=-1.0) == 1
+    assert sim(wsb=8) == 4
+    assert sim(ws=8) == 3
