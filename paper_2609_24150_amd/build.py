@@ -30,7 +30,7 @@ COMMON_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
     f"-I{INCLUDE}", f"-I{CSRC}",
-]
+] + os.environ.get("AAL_EXTRA_HIPCC_FLAGS", "").split()
 
 
 def hipcc() -> str:

@@ -83,8 +83,11 @@ aal_status_t validate_common(const CommonIn& c) {
   return AAL_OK;
 }
 
-aal_status_t run_loss(aal::LossArgs& a) {
-  hipError_t e = aal::launch_streaming(a);
+aal_status_t run_loss(aal::LossArgs& a, uint32_t flags) {
+  bool used = false;
+  hipError_t e = hipSuccess;
+  if (!(flags & AAL_FLAG_STREAMING)) e = aal::launch_resident(a, &used);
+  if (e == hipSuccess && !used) e = aal::launch_streaming(a);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
 }
@@ -148,7 +151,7 @@ aal_status_t aal_eal_fwd_bwd(const void* z_draft, const void* z_target, aal_dtyp
   a.grad = grad_draft;
   a.grad_scale = grad_scale;
   a.stream = static_cast<hipStream_t>(stream);
-  return run_loss(a);
+  return run_loss(a, flags);
 }
 
 aal_status_t aal_wtv_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N, int32_t K,
@@ -187,7 +190,7 @@ aal_status_t aal_wtv_fwd_bwd(const void* z_draft, const void* z_target, aal_dtyp
   a.grad = grad_draft;
   a.grad_scale = grad_scale;
   a.stream = static_cast<hipStream_t>(stream);
-  return run_loss(a);
+  return run_loss(a, flags);
 }
 
 aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int32_t P,

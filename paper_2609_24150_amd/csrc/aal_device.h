@@ -61,12 +61,13 @@ static __device__ __forceinline__ uint4 ldvec_nt(const void* base, int64_t vi) {
   return to_uint4(__builtin_nontemporal_load(static_cast<const u32x4*>(base) + vi));
 }
 
-// Gradient element types.  bf16 stores round to nearest even.
+// Gradient element types.  bf16 stores round to nearest even (one
+// v_cvt_pk_bf16_f32 per pair).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 static __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  __bf16 a = static_cast<__bf16>(lo);
-  __bf16 b = static_cast<__bf16>(hi);
-  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
-         (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 struct GBf16 {
@@ -156,6 +157,61 @@ static __device__ __forceinline__ float wave_sum(float v) {
   v = v + dppf<0x142, 0xA>(v, 0.f);
   v = v + dppf<0x143, 0xC>(v, 0.f);
   return readlane63(v);
+}
+
+// The same reductions over N independent values at once: every DPP step is
+// applied to all N values before the next, so DPP data hazards are covered by
+// independent work instead of s_nop.  Results are uniform across the wave.
+template <int N>
+static __device__ __forceinline__ void wave_max_n(float (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0xB1>(v[i], kNegInf));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0x4E>(v[i], kNegInf));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0x141>(v[i], kNegInf));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0x140>(v[i], kNegInf));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0x142, 0xA>(v[i], kNegInf));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0x143, 0xC>(v[i], kNegInf));
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = readlane63(v[i]);
+}
+
+template <int N>
+static __device__ __forceinline__ void wave_sum_n(float (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0xB1>(v[i], 0.f);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0x4E>(v[i], 0.f);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0x141>(v[i], 0.f);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0x140>(v[i], 0.f);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0x142, 0xA>(v[i], 0.f);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0x143, 0xC>(v[i], 0.f);
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = readlane63(v[i]);
+}
+
+// Wave merge of N (msc, sum) pairs: msc <- max over lanes (the wave's
+// reference), sum <- sum over lanes of sum * 2^(msc_lane - msc).
+template <int N>
+static __device__ __forceinline__ void wave_lse_n(float (&msc)[N], float (&s)[N]) {
+  float M[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) M[i] = msc[i];
+  wave_max_n(M);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    s[i] = (M[i] == kNegInf) ? 0.f : s[i] * ex2(msc[i] - M[i]);
+    msc[i] = M[i];
+  }
+  wave_sum_n(s);
 }
 
 // Integer min and fp64 sums are needed once per row only: a butterfly through

@@ -81,6 +81,14 @@ struct LossArgs {
 // gradient pass.  Handles every shape.
 hipError_t launch_streaming(const LossArgs& a);
 
+// loss = -(1/N) sum_n window_e[n], one workgroup, fixed summation order.
+hipError_t launch_loss_reduce(const LossArgs& a);
+
+// Register-resident single-kernel schedule.  Sets *used = false (and enqueues
+// nothing) when the shape is outside what it supports: V not a multiple of the 16-byte vector, K outside {1..8, 16}, a window too
+// wide for the co-resident grid, or no cooperative launch on the device.
+hipError_t launch_resident(const LossArgs& a, bool* used);
+
 struct SimArgs {
   DType in;
   const void* zd;

@@ -1,0 +1,705 @@
+// Register-resident schedule for the EAL and WTV losses: one kernel that reads
+// each logit once and writes the gradient once.
+//
+// A window (K logit rows) is split by vocabulary columns over a team of W
+// workgroups.  Each workgroup loads its column chunk of all K rows of both
+// logit tensors into VGPRs (16-byte nontemporal loads) and keeps them there:
+//
+//   phase A  per-row max / sum-exp partials of the tempered draft and target
+//            (EAL: greedy-token partial instead of the target sum);
+//            published to the team through the workspace, team barrier 1.
+//   phase B  every member merges the W partials in member order (so every
+//            member holds bit-identical row normalisers).
+//            WTV: per-row partial sums of min(p, q) and Q< = sum_{q<p} q,
+//            published, team barrier 2, merged in member order.
+//            EAL: a = q(x*) from the one logit z_draft[x*] re-read from HBM.
+//   scan     prefix products / suffix sums over the K rows give E and the
+//            gradient coefficients (Eqs. eal_generic, loss_eal, loss_tv).
+//   phase C  gradient from the registers, 16-byte nontemporal stores; each
+//            register slot is refilled with the team's next window as soon
+//            as its gradient is written, so loads overlap the stores.
+//
+// The grid is persistent and launched cooperatively, so every member of a
+// team is resident.  Partials travel as 64-bit words {value, tag}: a reader
+// polls the words it needs until every tag names the current window and
+// phase, so publishing doubles as the team barrier and no separate counter
+// round trip is needed.  Slots are double-buffered by window parity, which
+// keeps a fast member from overwriting a partial a slow member has not read.
+// Polls are bounded (a timeout sets an error word and the loss becomes NaN;
+// the kernel always exits).  Team members share blockIdx % 8, i.e. one XCD,
+// so the exchange stays in one L2.
+#include "aal_device.h"
+#include "aal_internal.h"
+
+#include <limits.h>
+
+#include <mutex>
+#include <type_traits>
+#include <vector>
+
+namespace aal {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kWaves = kBlock / kWave;
+#ifndef AAL_SLOT_BUDGET
+#define AAL_SLOT_BUDGET 16
+#endif
+// 16-byte vectors of each logit tensor a thread keeps per window (K * NV).
+constexpr int kSlotBudget = AAL_SLOT_BUDGET;
+constexpr unsigned kSpinLimit = 1u << 22;  // polls (~1 us each): seconds, far above any legitimate wait
+
+struct ResParams {
+  const uint8_t* zd;
+  const uint8_t* zt;
+  uint8_t* grad;
+  int64_t N;
+  int ng;              // 16-byte vectors per row
+  int W;               // workgroups per team
+  int T;               // teams
+  uint32_t row_bytes;  // bytes per logit row
+  uint32_t grow_bytes; // bytes per gradient row
+  float scd, sct, inv_t_d;
+  const float* grad_scale;
+  float* window_e;
+  float* accept;
+  int32_t* xstar;
+  uint64_t* slots;     // [parity 2][phase 2][T][K][W][4] words {value bits, tag}
+  unsigned* err;       // [1]
+};
+
+// The operand is the whole 128-bit tuple, so the data stays in the register
+// quadruple the 16-byte loads write (unpacked copies are not kept live across
+// phases, which would double the register footprint).
+__device__ __forceinline__ void pin(u32x4& x) { asm volatile("" : "+v"(x)); }
+
+__device__ __forceinline__ u32x4 neg_inf_vec(Bf16) { return u32x4{0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u}; }
+__device__ __forceinline__ u32x4 neg_inf_vec(F32) { return u32x4{0xff800000u, 0xff800000u, 0xff800000u, 0xff800000u}; }
+
+// Buffer resources: a wave-uniform 128-bit descriptor (base, byte range) in
+// SGPRs.  Accesses take a 32-bit per-lane byte offset plus an SGPR offset,
+// so no per-access 64-bit address arithmetic is needed.  For a raw buffer the
+// per-lane offset is range-checked: a store at or past the range is dropped.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRawBufferWord3 = 0x00020000;  // gfx9 raw (untyped) dword access
+constexpr int kNontemporal = 2;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), int(bytes), kRawBufferWord3);
+}
+__device__ __forceinline__ u32x4 bld16(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kNontemporal);
+}
+
+// One vector of gradient values at per-lane byte offset `off` of a row.
+template <class TG, int E>
+__device__ __forceinline__ void store_g(rsrc_t r, uint32_t off, const float (&g)[E]) {
+  if constexpr (sizeof(typename TG::storage) == 2 && E == 8) {
+    const u32x4 w = {pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]), pack_bf16x2(g[4], g[5]),
+                     pack_bf16x2(g[6], g[7])};
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, kNontemporal);
+  } else if constexpr (sizeof(typename TG::storage) == 2 && E == 4) {
+    const u32x2 w = {pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])};
+    __builtin_amdgcn_raw_buffer_store_b64(w, r, off, 0, kNontemporal);
+  } else if constexpr (E == 4) {
+    const u32x4 w = {__builtin_bit_cast(uint32_t, g[0]), __builtin_bit_cast(uint32_t, g[1]),
+                     __builtin_bit_cast(uint32_t, g[2]), __builtin_bit_cast(uint32_t, g[3])};
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, kNontemporal);
+  } else {
+    const u32x4 w0 = {__builtin_bit_cast(uint32_t, g[0]), __builtin_bit_cast(uint32_t, g[1]),
+                      __builtin_bit_cast(uint32_t, g[2]), __builtin_bit_cast(uint32_t, g[3])};
+    const u32x4 w1 = {__builtin_bit_cast(uint32_t, g[4]), __builtin_bit_cast(uint32_t, g[5]),
+                      __builtin_bit_cast(uint32_t, g[6]), __builtin_bit_cast(uint32_t, g[7])};
+    __builtin_amdgcn_raw_buffer_store_b128(w0, r, off, 0, kNontemporal);
+    __builtin_amdgcn_raw_buffer_store_b128(w1, r, off + 16u, 0, kNontemporal);
+  }
+}
+
+// One gradient value (through the same buffer path, so it lands after an
+// earlier vector store of the same thread to the same address).
+template <class TG>
+__device__ __forceinline__ void store_one(rsrc_t r, uint32_t off, float g) {
+  if constexpr (sizeof(typename TG::storage) == 2) {
+    const __bf16 h = static_cast<__bf16>(g);
+    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, h), r, off, 0, 0);
+  } else {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, g), r, off, 0, 0);
+  }
+}
+
+template <class TI, int E>
+__device__ __forceinline__ void unpackv(const u32x4& w, float (&x)[E]) {
+  TI::unpack(make_uint4(w.x, w.y, w.z, w.w), x);
+}
+
+__device__ __forceinline__ uint64_t tagged(float v, uint32_t tag) {
+  return (uint64_t(tag) << 32) | __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ void publish(uint64_t* p, float v, uint32_t tag) {
+  __hip_atomic_store(p, tagged(v, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t peek(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float value_of(uint64_t x) { return __builtin_bit_cast(float, uint32_t(x)); }
+
+// Reads the N consecutive tagged words at p, waiting until all carry `tag`.
+template <int N>
+__device__ __forceinline__ void collect(const uint64_t* p, uint32_t tag, unsigned* err, float (&out)[N]) {
+  uint64_t x[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = peek(p + i);
+  unsigned spins = 0;
+  for (;;) {
+    bool ok = true;
+#pragma unroll
+    for (int i = 0; i < N; ++i) ok = ok && uint32_t(x[i] >> 32) == tag;
+    if (ok) break;
+    if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) break;
+    if (++spins > kSpinLimit) {
+      __hip_atomic_store(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] = peek(p + i);
+  }
+#pragma unroll
+  for (int i = 0; i < N; ++i) out[i] = value_of(x[i]);
+}
+
+// Merge (msc, s) into (m, acc): references are fl(max * sc), monotone in max.
+__device__ __forceinline__ void lse_fold(float& m, float& acc, float msc, float s) {
+  const float nm = fmaxf(m, msc);
+  if (nm != kNegInf) {
+    acc = acc * ex2(m - nm) + s * ex2(msc - nm);
+    m = nm;
+  }
+}
+// Merge (value, index) keeping the larger value, then the lower index.
+__device__ __forceinline__ void argmax_fold(float& bv, float& bi, float v, float i) {
+  if (v > bv || (v == bv && __builtin_bit_cast(int, i) < __builtin_bit_cast(int, bi))) {
+    bv = v;
+    bi = i;
+  }
+}
+
+template <class TI, class TG, int MODE, int K, int NV>
+__global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
+  constexpr int E = TI::kVec;
+  constexpr bool kWtv = MODE == int(Mode::kWtv);
+  constexpr int GS = sizeof(typename TG::storage);  // gradient element bytes
+  static_assert(4 * K <= kWave, "one publishing lane per row component");
+  __shared__ float sh_w[kWaves][K][4];  // per-wave partials
+  __shared__ float sh_row[K][4];        // merged row constants
+  __shared__ float sh_coef[K][2];       // gradient coefficients
+  __shared__ int sh_x[K];
+
+  const int b = blockIdx.x;
+  int team, member;
+  if ((p.T & 7) == 0) {
+    const int j = b >> 3;
+    team = (j / p.W) * 8 + (b & 7);
+    member = j % p.W;
+  } else {
+    team = b / p.W;
+    member = b % p.W;
+  }
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wv = tid / kWave;
+  const bool last = member == p.W - 1;  // the only member whose chunk can pass the row end
+  int col[NV];
+  uint32_t coff[NV];  // clamped byte offsets of the slots within a row: always in bounds
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    col[v] = member * (kBlock * NV) + v * kBlock + tid;
+    coff[v] = uint32_t(min(col[v], p.ng - 1)) * 16u;
+  }
+  const int64_t stride_w = int64_t(K) * p.row_bytes;
+  uint64_t* const slots_team = p.slots + (int64_t(team) * K * p.W) * 4;
+  const int64_t slot_phase = int64_t(p.T) * K * p.W * 4;  // words per (parity, phase) plane
+
+  u32x4 rd[K][NV], rt[K][NV];
+
+  const uint32_t win_bytes = uint32_t(stride_w);
+  auto load_window = [&](int64_t w) {
+    const rsrc_t bd = make_rsrc(p.zd + w * stride_w, win_bytes);
+    const rsrc_t bt = make_rsrc(p.zt + w * stride_w, win_bytes);
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        rd[k][v] = bld16(bd, coff[v], k * p.row_bytes);
+        rt[k][v] = bld16(bt, coff[v], k * p.row_bytes);
+      }
+  };
+  auto pin_all = [&]() {
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        pin(rd[k][v]);
+        pin(rt[k][v]);
+      }
+  };
+
+  int64_t w = team;
+  if (w < p.N) load_window(w);
+  uint32_t iter = 0;
+  for (; w < p.N; w += p.T, ++iter) {
+    const int parity = iter & 1;
+    const uint32_t tagA = 2u * (iter + 1u), tagB = tagA + 1u;
+    uint64_t* const slotsA = slots_team + (2 * parity + 0) * slot_phase;
+    uint64_t* const slotsB = slots_team + (2 * parity + 1) * slot_phase;
+
+    // ------------------------------------------------------------ phase A
+    pin_all();
+    if (last) {  // slots past the row end hold copies of its last vector: mask them
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+        if (col[v] >= p.ng)
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            rd[k][v] = neg_inf_vec(TI{});
+            rt[k][v] = neg_inf_vec(TI{});
+          }
+    }
+    float m0[K], s0[K], m1[K], s1[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      float xs[NV][E];
+#pragma unroll
+      for (int v = 0; v < NV; ++v) unpackv<TI, E>(rd[k][v], xs[v]);
+      float m = kNegInf;
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < E; ++e) m = fmaxf(m, xs[v][e]);
+      const float msc = m * p.scd;
+      float sum = 0.f;
+      if (m != kNegInf) {
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int e = 0; e < E; ++e) sum += ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
+      }
+      m0[k] = m == kNegInf ? kNegInf : msc;
+      s0[k] = sum;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
+      if constexpr (kWtv) {
+        float mt = kNegInf;
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+        const float mtsc = mt * p.sct;
+        float st = 0.f;
+        if (mt != kNegInf) {
+#pragma unroll
+          for (int v = 0; v < NV; ++v)
+#pragma unroll
+            for (int e = 0; e < E; ++e) st += ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+        }
+        m1[k] = mt == kNegInf ? kNegInf : mtsc;
+        s1[k] = st;
+      } else {
+        float best = kNegInf;
+        int bidx = INT_MAX;
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int e = 0; e < E; ++e)
+            if (xs[v][e] > best) {
+              best = xs[v][e];
+              bidx = col[v] * E + e;
+            }
+        m1[k] = best;
+        s1[k] = __builtin_bit_cast(float, bidx);
+      }
+    }
+    wave_lse_n(m0, s0);
+    if constexpr (kWtv) {
+      wave_lse_n(m1, s1);
+    } else {
+      float bv[K];
+#pragma unroll
+      for (int k = 0; k < K; ++k) bv[k] = m1[k];
+      wave_max_n(bv);
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int bi = (m1[k] == bv[k]) ? __builtin_bit_cast(int, s1[k]) : INT_MAX;
+        s1[k] = __builtin_bit_cast(float, wave_min_i(bi));
+        m1[k] = bv[k];
+      }
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        sh_w[wv][k][0] = m0[k];
+        sh_w[wv][k][1] = s0[k];
+        sh_w[wv][k][2] = m1[k];
+        sh_w[wv][k][3] = s1[k];
+      }
+    }
+    __syncthreads();
+    if (tid < 4 * K) {  // merge the 4 waves (fixed order), publish one component each
+      const int k = tid >> 2, c = tid & 3;
+      float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
+#pragma unroll
+      for (int i = 1; i < kWaves; ++i) {
+        lse_fold(a0, a1, sh_w[i][k][0], sh_w[i][k][1]);
+        if constexpr (kWtv) {
+          lse_fold(a2, a3, sh_w[i][k][2], sh_w[i][k][3]);
+        } else {
+          argmax_fold(a2, a3, sh_w[i][k][2], sh_w[i][k][3]);
+        }
+      }
+      const float val = c == 0 ? a0 : c == 1 ? a1 : c == 2 ? a2 : a3;
+      publish(slotsA + (int64_t(k) * p.W + member) * 4 + c, val, tagA);
+    }
+
+    // ------------------------------------------------------------ phase B
+    // Row merges: wave wv takes rows wv, wv+4, ...; lane j folds members j,
+    // j+64, ... in order, then a fixed DPP tree: every member of the team
+    // obtains bit-identical row constants.
+    for (int k = wv; k < K; k += kWaves) {
+      float a0[1] = {kNegInf}, a1[1] = {0.f}, a2[1] = {kNegInf}, a3[1];
+      a3[0] = kWtv ? 0.f : __builtin_bit_cast(float, INT_MAX);
+      for (int j = lane; j < p.W; j += kWave) {
+        float q[4];
+        collect<4>(slotsA + (int64_t(k) * p.W + j) * 4, tagA, p.err, q);
+        lse_fold(a0[0], a1[0], q[0], q[1]);
+        if constexpr (kWtv) {
+          lse_fold(a2[0], a3[0], q[2], q[3]);
+        } else {
+          argmax_fold(a2[0], a3[0], q[2], q[3]);
+        }
+      }
+      wave_lse_n(a0, a1);
+      if constexpr (kWtv) {
+        wave_lse_n(a2, a3);
+        if (lane == 0) {
+          sh_row[k][0] = a0[0];
+          sh_row[k][1] = __log2f(a1[0]);
+          sh_row[k][2] = a2[0];
+          sh_row[k][3] = __log2f(a3[0]);
+        }
+      } else {
+        float bv[1] = {a2[0]};
+        wave_max_n(bv);
+        int x = wave_min_i(a2[0] == bv[0] ? __builtin_bit_cast(int, a3[0]) : INT_MAX);
+        if (lane == 0) {
+          if (x == INT_MAX) x = 0;  // no finite target logit: unspecified, stay in bounds
+          const float l2s = __log2f(a1[0]);
+          const float zx = TI::load1(p.zd + (w * K + k) * int64_t(p.row_bytes), x);
+          sh_x[k] = x;
+          sh_row[k][0] = a0[0];
+          sh_row[k][1] = l2s;
+          sh_row[k][2] = ex2(__builtin_fmaf(zx, p.scd, -a0[0]) - l2s);  // a = q(x*)
+        }
+      }
+    }
+    __syncthreads();
+
+    if constexpr (kWtv) {
+      pin_all();
+      float am[K], aq[K];
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const float mscd = sh_row[k][0], l2sd = sh_row[k][1];
+        const float msct = sh_row[k][2], l2st = sh_row[k][3];
+        float sm = 0.f, sq = 0.f;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          float xd[E], xt[E];
+          unpackv<TI, E>(rd[k][v], xd);
+          unpackv<TI, E>(rt[k][v], xt);
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const float ld = __builtin_fmaf(xd[e], p.scd, -mscd) - l2sd;
+            const float lt = __builtin_fmaf(xt[e], p.sct, -msct) - l2st;
+            const float mn = ex2(fminf(ld, lt));
+            sm += mn;
+            sq += (ld < lt) ? mn : 0.f;
+          }
+        }
+        am[k] = sm;
+        aq[k] = sq;
+      }
+      wave_sum_n(am);
+      wave_sum_n(aq);
+      if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          sh_w[wv][k][0] = am[k];
+          sh_w[wv][k][1] = aq[k];
+        }
+      }
+      __syncthreads();
+      if (tid < 2 * K) {
+        const int k = tid >> 1, c = tid & 1;
+        float r = sh_w[0][k][c];
+#pragma unroll
+        for (int i = 1; i < kWaves; ++i) r += sh_w[i][k][c];
+        publish(slotsB + (int64_t(k) * p.W + member) * 4 + c, r, tagB);
+      }
+      for (int k = wv; k < K; k += kWaves) {
+        float r[2] = {0.f, 0.f};
+        for (int j = lane; j < p.W; j += kWave) {
+          float q[2];
+          collect<2>(slotsB + (int64_t(k) * p.W + j) * 4, tagB, p.err, q);
+          r[0] += q[0];
+          r[1] += q[1];
+        }
+        wave_sum_n(r);
+        if (lane == 0) {
+          sh_coef[k][0] = r[0];  // a_k, until the scan below
+          sh_coef[k][1] = r[1];  // Q<_k
+        }
+      }
+      __syncthreads();
+    }
+
+    // --------------------------------------------------------------- scan
+    if (tid == 0) {
+      float a[K], qlt[K];
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        a[k] = kWtv ? sh_coef[k][0] : sh_row[k][2];
+        qlt[k] = kWtv ? sh_coef[k][1] : 0.f;
+      }
+      double Pp[K];
+      double pr = 1.0, Ew = 0.0;
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        Pp[k] = pr;
+        pr *= double(a[k]);
+        Ew += pr;
+      }
+      const double scale = p.grad_scale ? double(*p.grad_scale) : 1.0;
+      const double inv_n = 1.0 / double(p.N);
+      double S = 1.0;
+#pragma unroll
+      for (int k = K - 1; k >= 0; --k) {
+        const double g = -Pp[k] * S * inv_n;
+        const double factor = kWtv ? double(p.inv_t_d) : double(a[k]) * double(p.inv_t_d);
+        const float c = float(g * scale * factor);
+        if constexpr (kWtv) {
+          sh_coef[k][0] = c * (1.f - qlt[k]);
+          sh_coef[k][1] = -c * qlt[k];
+        } else {
+          sh_coef[k][0] = c;
+        }
+        S = 1.0 + double(a[k]) * S;
+      }
+      if (member == 0) {
+        p.window_e[w] = float(Ew);
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          if (p.accept) p.accept[w * K + k] = a[k];
+          if constexpr (!kWtv) {
+            if (p.xstar) p.xstar[w * K + k] = sh_x[k];
+          }
+        }
+      }
+    }
+    __syncthreads();
+
+    // ------------------------------------------------------------ phase C
+    // Gradient from the registers; each slot is refilled with the team's next
+    // window right after its gradient is stored.
+    const int64_t wn = w + p.T;
+    const bool more = wn < p.N;
+    const rsrc_t nd = make_rsrc(p.zd + (more ? wn : w) * stride_w, win_bytes);
+    const rsrc_t nt = make_rsrc(p.zt + (more ? wn : w) * stride_w, win_bytes);
+    uint8_t* const gw = p.grad ? p.grad + w * int64_t(K) * p.grow_bytes : nullptr;
+    pin_all();
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const float mscd = sh_row[k][0], l2sd = sh_row[k][1];
+      float msct = 0.f, l2st = 0.f, cA, cB = 0.f;
+      int xk = 0;
+      if constexpr (kWtv) {
+        msct = sh_row[k][2];
+        l2st = sh_row[k][3];
+        cA = sh_coef[k][0];
+        cB = sh_coef[k][1];
+      } else {
+        cA = sh_coef[k][0];
+        xk = sh_x[k];
+      }
+      uint8_t* const gk = gw + k * p.grow_bytes;
+      const rsrc_t gr = make_rsrc(gk, p.grow_bytes);  // slots past the row end are dropped
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        if (gw != nullptr) {
+          float xd[E], g[E];
+          unpackv<TI, E>(rd[k][v], xd);
+          if constexpr (kWtv) {
+            float xt[E];
+            unpackv<TI, E>(rt[k][v], xt);
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+              const float ld = __builtin_fmaf(xd[e], p.scd, -mscd) - l2sd;
+              const float lt = __builtin_fmaf(xt[e], p.sct, -msct) - l2st;
+              g[e] = ex2(ld) * ((ld < lt) ? cA : cB);
+            }
+          } else {
+            // -c q everywhere; the greedy token's entry is fixed up after the loop
+#pragma unroll
+            for (int e = 0; e < E; ++e) g[e] = -cA * ex2(__builtin_fmaf(xd[e], p.scd, -mscd) - l2sd);
+          }
+          store_g<TG, E>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
+        }
+        asm volatile("" ::: "memory");  // keep the refill below this slot's store
+        if (more) {
+          rd[k][v] = bld16(nd, coff[v], k * p.row_bytes);
+          rt[k][v] = bld16(nt, coff[v], k * p.row_bytes);
+        }
+      }
+    }
+    if constexpr (!kWtv) {
+      // EAL: the greedy token's entry is c (1 - q(x*)) = c (1 - a), written by
+      // the thread whose vector store covered it (same thread, so it lands last)
+      if (gw != nullptr) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int xk = sh_x[k];
+          bool own = false;
+#pragma unroll
+          for (int v = 0; v < NV; ++v) own = own || (col[v] == xk / E);
+          if (own) {
+            const rsrc_t gr = make_rsrc(gw + k * p.grow_bytes, p.grow_bytes);
+            store_one<TG>(gr, uint32_t(xk) * GS, sh_coef[k][0] * (1.f - sh_row[k][2]));
+          }
+        }
+      }
+    }
+    __syncthreads();  // sh_row / sh_coef are rewritten by the next window
+  }
+}
+
+// Marks the loss NaN if any poll timed out.
+__global__ void k_poison_loss(const unsigned* err, float* loss) {
+  if (threadIdx.x == 0 && *err != 0u) loss[0] = __builtin_nanf("");
+}
+
+// Zeroes the tag words (tag 0 never matches) and the error word.
+__global__ void k_clear(uint64_t* p, int64_t n) {
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+    p[i] = 0;
+}
+
+// -------------------------------------------------------------- dispatch
+struct DevInfo {
+  int cus = 0;
+  bool coop = false;
+};
+
+DevInfo device_info() {
+  static std::mutex mu;
+  static std::vector<DevInfo> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return {};
+  std::lock_guard<std::mutex> lk(mu);
+  if (int(cache.size()) <= dev) cache.resize(dev + 1);
+  if (cache[dev].cus == 0) {
+    int cus = 0, coop = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return {};
+    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess) return {};
+    cache[dev] = {cus, coop != 0};
+  }
+  return cache[dev];
+}
+
+template <class TI, class TG, int MODE, int K>
+hipError_t launch_k(const LossArgs& a, bool* used) {
+  constexpr int NV = (kSlotBudget / K) > 0 ? (kSlotBudget / K) : 1;
+  constexpr int E = TI::kVec;
+  auto kern = k_resident<TI, TG, MODE, K, NV>;
+  const DevInfo di = device_info();
+  if (!di.coop || di.cus == 0) return hipSuccess;
+  const int ng = a.V / E;
+  const int W = (ng + kBlock * NV - 1) / (kBlock * NV);
+  const int64_t row_bytes = int64_t(a.V) * (a.in == DType::kBf16 ? 2 : 4);
+  const int64_t grow_bytes = int64_t(a.V) * (a.gd == DType::kBf16 ? 2 : 4);
+  if (int64_t(K) * grow_bytes >= (int64_t(1) << 31) || int64_t(K) * row_bytes >= (int64_t(1) << 31))
+    return hipSuccess;  // 32-bit in-window offsets
+  int per_cu = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kBlock, 0);
+  if (e != hipSuccess) return e;
+  const int64_t resident = int64_t(per_cu) * di.cus;
+  int64_t T = resident / W;
+  if (T >= 8) T -= T % 8;
+  if (T > a.N) T = a.N;
+  if (T < 1) return hipSuccess;  // a window does not fit: streaming schedule
+  auto words = [&](int64_t t) { return int64_t(2) * 2 * t * K * W * 4; };
+  while (T > 8 && size_t(words(T) + 1) * 8 > a.ws.resident_bytes) T -= 8;
+  if (size_t(words(T) + 1) * 8 > a.ws.resident_bytes) return hipSuccess;
+  ResParams p{};
+  p.zd = static_cast<const uint8_t*>(a.zd);
+  p.zt = static_cast<const uint8_t*>(a.zt);
+  p.grad = static_cast<uint8_t*>(a.grad);
+  p.N = a.N;
+  p.ng = ng;
+  p.W = W;
+  p.T = int(T);
+  p.row_bytes = uint32_t(row_bytes);
+  p.grow_bytes = uint32_t(grow_bytes);
+  p.scd = a.sc_d;
+  p.sct = a.sc_t;
+  p.inv_t_d = a.inv_t_d;
+  p.grad_scale = a.grad_scale;
+  p.window_e = a.window_e;
+  p.accept = a.accept;
+  p.xstar = a.xstar;
+  p.slots = reinterpret_cast<uint64_t*>(a.ws.resident);
+  p.err = reinterpret_cast<unsigned*>(p.slots + words(T));
+  const int64_t nclear = words(T) + 1;
+  k_clear<<<64, kBlock, 0, a.stream>>>(p.slots, nclear);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  void* args[] = {&p};
+  e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(unsigned(T * W)), dim3(kBlock), args, 0,
+                                 a.stream);
+  if (e != hipSuccess) return e;
+  *used = true;
+  if ((e = launch_loss_reduce(a)) != hipSuccess) return e;
+  k_poison_loss<<<1, 64, 0, a.stream>>>(p.err, a.loss);
+  return hipGetLastError();
+}
+
+template <class TI, class TG, int MODE>
+hipError_t launch_mode(const LossArgs& a, bool* used) {
+  switch (a.K) {
+    case 1: return launch_k<TI, TG, MODE, 1>(a, used);
+    case 2: return launch_k<TI, TG, MODE, 2>(a, used);
+    case 3: return launch_k<TI, TG, MODE, 3>(a, used);
+    case 4: return launch_k<TI, TG, MODE, 4>(a, used);
+    case 5: return launch_k<TI, TG, MODE, 5>(a, used);
+    case 6: return launch_k<TI, TG, MODE, 6>(a, used);
+    case 7: return launch_k<TI, TG, MODE, 7>(a, used);
+    case 8: return launch_k<TI, TG, MODE, 8>(a, used);
+    case 16: return launch_k<TI, TG, MODE, 16>(a, used);
+    default: return hipSuccess;
+  }
+}
+
+template <class TI>
+hipError_t launch_in(const LossArgs& a, bool* used) {
+  const bool bf_grad = a.gd == DType::kBf16;
+  if (a.mode == Mode::kEal)
+    return bf_grad ? launch_mode<TI, GBf16, int(Mode::kEal)>(a, used) : launch_mode<TI, GF32, int(Mode::kEal)>(a, used);
+  return bf_grad ? launch_mode<TI, GBf16, int(Mode::kWtv)>(a, used) : launch_mode<TI, GF32, int(Mode::kWtv)>(a, used);
+}
+
+}  // namespace
+
+hipError_t launch_resident(const LossArgs& a, bool* used) {
+  *used = false;
+  const int E = a.in == DType::kBf16 ? Bf16::kVec : F32::kVec;
+  if (a.V % E != 0) return hipSuccess;
+  return a.in == DType::kBf16 ? launch_in<Bf16>(a, used) : launch_in<F32>(a, used);
+}
+
+}  // namespace aal

@@ -343,6 +343,11 @@ hipError_t launch_typed(const LossArgs& a) {
 
 }  // namespace
 
+hipError_t launch_loss_reduce(const LossArgs& a) {
+  k_loss<<<1, kBlock, 0, a.stream>>>(a.window_e, a.N, a.loss);
+  return hipGetLastError();
+}
+
 hipError_t launch_streaming(const LossArgs& a) {
   if (a.in == DType::kBf16) {
     return a.mode == Mode::kEal ? launch_typed<Bf16, int(Mode::kEal)>(a) : launch_typed<Bf16, int(Mode::kWtv)>(a);
