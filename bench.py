@@ -29,6 +29,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+PMC_PROFILE = os.path.join(ROOT, "profiles", "resident_wtv_c2_pmc.txt")
+KERNEL_SOURCES = ["paper_2609_24150_amd/csrc/aal_resident.hip", "paper_2609_24150_amd/csrc/aal_device.h",
+                  "paper_2609_24150_amd/csrc/aal_internal.h"]
 WORKLOAD_TEXT = {
     "c2": "WTV fwd+bwd: N=2048 windows x K=7 x V=128256, bf16 logits, bf16 grad, T=1.0/1.0",
     "c4": "WTV fwd+bwd: N=16384 windows x K=16 x V=32000, fp32 logits, fp32 grad, T=0.5/0.5",
@@ -80,6 +83,26 @@ def cpu_baseline(workload: str, budget_s: float = 12.0) -> dict:
     return {"value": rate, "unit": "logit rows/s", "cores": workers, "kind": "oracle",
             "sample": f"{workers} processes x {nwin} windows of the workload (K={K}, V={V}), each repeated "
                       f"for ~{budget_s:.0f}s; {rows} rows in {wall:.1f}s wall"}
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the fused kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None when that summary does not cover
+    this workload or the kernel sources changed since it was taken."""
+    import hashlib
+    if workload != "c2" or not os.path.exists(PMC_PROFILE):
+        return None
+    fields = {}
+    for line in open(PMC_PROFILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.split()[0]
+    h = hashlib.sha256()
+    for src in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, src), "rb").read())
+    if fields.get("kernel_source_sha256") != h.hexdigest():
+        return None
+    return float(fields["traffic_bytes_per_launch"])
 
 
 # ----------------------------------------------------------------- GPU legs
@@ -171,6 +194,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-also", action="store_true", help="skip the secondary EAL and simulation legs")
     ap.add_argument("--flags", type=int, default=0, help="AAL_FLAG_* bits for the timed call")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed steps, run one device copy of 4 GiB (a reference kernel of known "
+                         "traffic for hardware-counter runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -212,10 +238,22 @@ def main():
         "config": {"workload": WORKLOAD_TEXT[args.workload], "N": N, "K": K, "V": V,
                    "windows_per_s": N / (ms * 1e-3)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
-                     "bytes_per_step": alg_bytes, "kernel": "whole aal_wtv_fwd_bwd call"},
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": measured_traffic(args.workload),
+                     "algorithmic_bytes": alg_bytes,
+                     "kernel": "k_resident (timed: the whole aal_wtv_fwd_bwd call, i.e. k_resident plus "
+                               "three microsecond-scale set-up/reduction kernels)"},
         "cpu_baseline": cpu,
     }
+    if args.copy_calibration:
+        src = torch.empty(1 << 32, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = {"read": 1 << 32, "write": 1 << 32}
+        del src, dst
+        torch.cuda.empty_cache()
     if not args.no_also:
         also = {}
         fn_e, st_e, _ = loss_call("eal", inp, gdt, args.flags)

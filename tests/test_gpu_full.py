@@ -1,0 +1,155 @@
+"""GPU parity at the five workloads' full sizes.
+
+The library runs on the whole workload (the same call bench.py times); the
+fp64 oracle recomputes a sample of windows (or GRPO groups) one by one and the
+outputs are compared there, with the tolerances of tests/parity.py.  Over all
+windows the loss must equal -mean(E) of the per-window outputs, and every E
+must lie in [0, K]."""
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from parity import check_grad, eal_coef, host64, loss_tol, rel_err, wtv_coef, wtv_flips
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def A():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_24150_amd as lib
+    return lib
+
+
+def _free():
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _sample(N, n=10, seed=0):
+    rng = np.random.default_rng(seed)
+    return np.unique(np.concatenate([[0, N - 1], rng.choice(N, size=n, replace=False)]))
+
+
+def _check_loss_consistency(r, K):
+    E = host64(r["E"])
+    assert np.all(np.isfinite(E)) and E.min() >= 0 and E.max() <= K * (1 + 1e-6)
+    assert rel_err(r["loss"].item(), -E.mean()) <= 1e-6
+
+
+def _run_eal(A, zd, zt, T, idx):
+    N, K, _ = zd.shape
+    r = A.aal_eal_fwd_bwd(zd, zt, T)
+    torch.cuda.synchronize()
+    _check_loss_consistency(r, K)
+    sel = torch.as_tensor(idx, device=zd.device)
+    zd_s, zt_s = host64(zd[sel]), host64(zt[sel])
+    o = O.eal_loss(zd_s, zt_s, T)
+    # the oracle's loss over the sample has 1/|sample|; rescale to the full 1/N
+    scale = len(idx) / N
+    assert np.array_equal(r["xstar"][sel].cpu().numpy(), o["xstar"])
+    tol = loss_tol(zd.dtype)
+    assert rel_err(host64(r["E"][sel]), o["E"]) <= tol
+    np.testing.assert_allclose(host64(r["accept"][sel]), o["a"], rtol=tol, atol=1e-7)
+    coef = eal_coef(o, len(idx), T) * scale
+    stats = check_grad(host64(r["grad"][sel]), o["grad"] * scale, coef, zd.dtype, zd.dtype)
+    del r
+    return stats
+
+
+def _run_wtv(A, zd, zt, Td, Tt, idx):
+    N, K, _ = zd.shape
+    r = A.aal_wtv_fwd_bwd(zd, zt, Td, Tt)
+    torch.cuda.synchronize()
+    _check_loss_consistency(r, K)
+    sel = torch.as_tensor(idx, device=zd.device)
+    zd_s, zt_s = host64(zd[sel]), host64(zt[sel])
+    o = O.wtv_loss(zd_s, zt_s, Td, Tt)
+    scale = len(idx) / N
+    tol = loss_tol(zd.dtype)
+    assert rel_err(host64(r["E"][sel]), o["E"]) <= tol
+    np.testing.assert_allclose(host64(r["accept"][sel]), o["a"], rtol=tol, atol=1e-6 if zd.dtype == torch.float32 else 1e-4)
+    coef = wtv_coef(o, len(idx), Td) * scale
+    rows, elems = wtv_flips(zd_s, zt_s, Td, Tt, coef)
+    stats = check_grad(host64(r["grad"][sel]), o["grad"] * scale, coef, zd.dtype, zd.dtype,
+                       exclude_rows=rows, exclude_elems=elems)
+    del r
+    return stats
+
+
+def test_c1_eal_fp32_full(A):
+    from paper_2609_24150_amd.inputs import make_config
+    d = make_config("c1", device="cuda")
+    zd, zt = d["z_draft"], d["z_target"]
+    r = A.aal_eal_fwd_bwd(zd, zt, 1.0)
+    torch.cuda.synchronize()
+    o = O.eal_loss(host64(zd), host64(zt), 1.0)
+    assert np.array_equal(r["xstar"].cpu().numpy(), o["xstar"])
+    assert rel_err(r["loss"].item(), o["loss"]) <= 1e-5
+    assert rel_err(host64(r["E"]), o["E"]) <= 1e-5
+    check_grad(host64(r["grad"]), o["grad"], eal_coef(o, 64, 1.0), torch.float32, torch.float32)
+
+
+def test_c2_wtv_and_eal_bf16_full(A):
+    from paper_2609_24150_amd.inputs import make_config
+    d = make_config("c2", device="cuda")
+    zd, zt = d["z_draft"], d["z_target"]
+    idx = _sample(2048, 10, seed=2)
+    _run_wtv(A, zd, zt, 1.0, 1.0, idx)
+    _run_eal(A, zd, zt, 1.0, idx)
+    del d, zd, zt
+    _free()
+
+
+def test_c3_eal_and_wtv_bf16_full(A):
+    from paper_2609_24150_amd.inputs import make_config
+    d = make_config("c3", device="cuda")
+    zd, zt = d["z_draft"], d["z_target"]
+    idx = _sample(4096, 10, seed=3)
+    _run_eal(A, zd, zt, 1.0, idx)
+    _run_wtv(A, zd, zt, 0.7, 0.7, idx)
+    del d, zd, zt
+    _free()
+
+
+def test_c4_wtv_fp32_full(A):
+    from paper_2609_24150_amd.inputs import make_config
+    d = make_config("c4", device="cuda")
+    zd, zt = d["z_draft"], d["z_target"]
+    idx = _sample(16384, 10, seed=4)
+    _run_wtv(A, zd, zt, 0.5, 0.5, idx)
+    del d, zd, zt
+    _free()
+
+
+def test_c5_sim_grpo_bf16_full(A):
+    from paper_2609_24150_amd.inputs import make_config
+    d = make_config("c5", device="cuda")
+    zd, zt, u1, u2 = d["z_draft"], d["z_target"], d["u1"], d["u2"]
+    P, G, K, V = zd.shape
+    r = A.aal_sim_accept_grpo(zd, zt, u1, u2, 1.0)
+    torch.cuda.synchronize()
+    rew = r["reward"].cpu().numpy()
+    assert rew.min() >= 0 and rew.max() <= K
+    adv = host64(r["advantage"])
+    np.testing.assert_allclose(adv.mean(-1), 0.0, atol=1e-5)
+    idx = _sample(P, 6, seed=5)
+    sel = torch.as_tensor(idx, device=zd.device)
+    zd_s, zt_s, u1_s, u2_s = host64(zd[sel]), host64(zt[sel]), host64(u1[sel]), host64(u2[sel])
+    o = O.sim_accept_grpo(zd_s, zt_s, 1.0, u1_s, u2_s)
+    flag = O.sim_near_threshold(zd_s, zt_s, 1.0, u1_s, u2_s)
+    tok = r["token"][sel].cpu().numpy()
+    acc = r["accept"][sel].cpu().numpy().astype(bool)
+    assert np.array_equal(tok[~flag], o["token"][~flag])
+    assert np.array_equal(acc[~flag], o["accept"][~flag])
+    first_rej = np.where(o["accept"].all(-1), K - 1, np.argmin(o["accept"], -1))
+    gflag = (flag & (np.arange(K)[None, None, :] <= first_rej[..., None])).any(-1)
+    assert np.array_equal(rew[idx][~gflag], o["reward"][~gflag])
+    pflag = gflag.any(-1)
+    np.testing.assert_allclose(adv[idx][~pflag], o["advantage"][~pflag], atol=1e-5, rtol=0)
+    del d, zd, zt
+    _free()
