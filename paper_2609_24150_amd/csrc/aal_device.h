@@ -135,6 +135,13 @@ static __device__ __forceinline__ float dppf(float v, float id) {
                                          RowMask, 0xF, false));
 }
 
+// Full-row-mask DPP move: every lane has a source lane for these patterns, so
+// no identity is needed and the move can fuse into the consuming ALU op.
+template <int Ctrl>
+static __device__ __forceinline__ float dppm(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), Ctrl, 0xF, 0xF, true));
+}
+
 static __device__ __forceinline__ float readlane63(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
@@ -165,13 +172,13 @@ static __device__ __forceinline__ float wave_sum(float v) {
 template <int N>
 static __device__ __forceinline__ void wave_max_n(float (&v)[N]) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0xB1>(v[i], kNegInf));
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppm<0xB1>(v[i]));
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0x4E>(v[i], kNegInf));
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppm<0x4E>(v[i]));
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0x141>(v[i], kNegInf));
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppm<0x141>(v[i]));
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0x140>(v[i], kNegInf));
+  for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppm<0x140>(v[i]));
 #pragma unroll
   for (int i = 0; i < N; ++i) v[i] = fmaxf(v[i], dppf<0x142, 0xA>(v[i], kNegInf));
 #pragma unroll
@@ -183,13 +190,13 @@ static __device__ __forceinline__ void wave_max_n(float (&v)[N]) {
 template <int N>
 static __device__ __forceinline__ void wave_sum_n(float (&v)[N]) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0xB1>(v[i], 0.f);
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppm<0xB1>(v[i]);
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0x4E>(v[i], 0.f);
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppm<0x4E>(v[i]);
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0x141>(v[i], 0.f);
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppm<0x141>(v[i]);
 #pragma unroll
-  for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0x140>(v[i], 0.f);
+  for (int i = 0; i < N; ++i) v[i] = v[i] + dppm<0x140>(v[i]);
 #pragma unroll
   for (int i = 0; i < N; ++i) v[i] = v[i] + dppf<0x142, 0xA>(v[i], 0.f);
 #pragma unroll

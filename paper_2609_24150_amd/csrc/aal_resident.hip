@@ -40,8 +40,7 @@
 namespace aal {
 namespace {
 
-constexpr int kBlock = 256;
-constexpr int kWaves = kBlock / kWave;
+constexpr int kClearBlock = 256;
 #ifndef AAL_SLOT_BUDGET
 #define AAL_SLOT_BUDGET 16
 #endif
@@ -183,8 +182,9 @@ __device__ __forceinline__ void argmax_fold(float& bv, float& bi, float v, float
   }
 }
 
-template <class TI, class TG, int MODE, int K, int NV>
+template <class TI, class TG, int MODE, int K, int NV, int kBlock>
 __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
+  constexpr int kWaves = kBlock / kWave;
   constexpr int E = TI::kVec;
   constexpr bool kWtv = MODE == int(Mode::kWtv);
   constexpr int GS = sizeof(typename TG::storage);  // gradient element bytes
@@ -405,10 +405,14 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     if constexpr (kWtv) {
       pin_all();
       float am[K], aq[K];
+      // With u, w the two fmas below, log2 q = u - l2sd and log2 p = w - l2st,
+      // so min(p, q) = 2^-l2sd 2^min(u, w - dl) and [q < p] = [u < w - dl] for
+      // dl = l2st - l2sd: the common factor is applied once per row after the
+      // reductions.
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        const float mscd = sh_row[k][0], l2sd = sh_row[k][1];
-        const float msct = sh_row[k][2], l2st = sh_row[k][3];
+        const float mscd = sh_row[k][0];
+        const float msct = sh_row[k][2], dl = sh_row[k][3] - sh_row[k][1];
         float sm = 0.f, sq = 0.f;
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
@@ -417,11 +421,11 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           unpackv<TI, E>(rt[k][v], xt);
 #pragma unroll
           for (int e = 0; e < E; ++e) {
-            const float ld = __builtin_fmaf(xd[e], p.scd, -mscd) - l2sd;
-            const float lt = __builtin_fmaf(xt[e], p.sct, -msct) - l2st;
-            const float mn = ex2(fminf(ld, lt));
+            const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
+            const float t = __builtin_fmaf(xt[e], p.sct, -msct) - dl;
+            const float mn = ex2(fminf(u, t));
             sm += mn;
-            sq += (ld < lt) ? mn : 0.f;
+            sq += (u < t) ? mn : 0.f;
           }
         }
         am[k] = sm;
@@ -442,7 +446,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         float r = sh_w[0][k][c];
 #pragma unroll
         for (int i = 1; i < kWaves; ++i) r += sh_w[i][k][c];
-        publish(slotsB + (int64_t(k) * p.W + member) * 4 + c, r, tagB);
+        publish(slotsB + (int64_t(k) * p.W + member) * 4 + c, r * ex2(-sh_row[k][1]), tagB);
       }
       for (int k = wv; k < K; k += kWaves) {
         float r[2] = {0.f, 0.f};
@@ -517,17 +521,19 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     pin_all();
 #pragma unroll
     for (int k = 0; k < K; ++k) {
-      const float mscd = sh_row[k][0], l2sd = sh_row[k][1];
-      float msct = 0.f, l2st = 0.f, cA, cB = 0.f;
-      int xk = 0;
+      // q = 2^-l2sd 2^u: the row factor 2^-l2sd is folded into the coefficients
+      const float mscd = sh_row[k][0], rs = ex2(-sh_row[k][1]);
+      float msct = 0.f, dl = 0.f, cA, cB = 0.f;
       if constexpr (kWtv) {
         msct = sh_row[k][2];
-        l2st = sh_row[k][3];
-        cA = sh_coef[k][0];
-        cB = sh_coef[k][1];
+        dl = sh_row[k][3] - sh_row[k][1];
+        cA = sh_coef[k][0] * rs;
+        cB = sh_coef[k][1] * rs;
+        // keep the products: the select below would otherwise absorb them and
+        // multiply every element by rs
+        asm volatile("" : "+v"(cA), "+v"(cB));
       } else {
-        cA = sh_coef[k][0];
-        xk = sh_x[k];
+        cA = -sh_coef[k][0] * rs;
       }
       uint8_t* const gk = gw + k * p.grow_bytes;
       const rsrc_t gr = make_rsrc(gk, p.grow_bytes);  // slots past the row end are dropped
@@ -541,14 +547,14 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
             unpackv<TI, E>(rt[k][v], xt);
 #pragma unroll
             for (int e = 0; e < E; ++e) {
-              const float ld = __builtin_fmaf(xd[e], p.scd, -mscd) - l2sd;
-              const float lt = __builtin_fmaf(xt[e], p.sct, -msct) - l2st;
-              g[e] = ex2(ld) * ((ld < lt) ? cA : cB);
+              const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
+              const float t = __builtin_fmaf(xt[e], p.sct, -msct) - dl;
+              g[e] = ex2(u) * ((u < t) ? cA : cB);
             }
           } else {
             // -c q everywhere; the greedy token's entry is fixed up after the loop
 #pragma unroll
-            for (int e = 0; e < E; ++e) g[e] = -cA * ex2(__builtin_fmaf(xd[e], p.scd, -mscd) - l2sd);
+            for (int e = 0; e < E; ++e) g[e] = cA * ex2(__builtin_fmaf(xd[e], p.scd, -mscd));
           }
           store_g<TG, E>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
         }
@@ -613,11 +619,20 @@ DevInfo device_info() {
   return cache[dev];
 }
 
+// Workgroup size per mode: WTV synchronises a team twice per window, so fewer,
+// wider members (512 threads, one workgroup per CU) pay less team skew; EAL
+// synchronises once and gains more from a second co-resident workgroup per CU.
+template <int MODE>
+constexpr int block_for() {
+  return MODE == int(Mode::kWtv) ? 512 : 256;
+}
+
 template <class TI, class TG, int MODE, int K>
 hipError_t launch_k(const LossArgs& a, bool* used) {
   constexpr int NV = (kSlotBudget / K) > 0 ? (kSlotBudget / K) : 1;
   constexpr int E = TI::kVec;
-  auto kern = k_resident<TI, TG, MODE, K, NV>;
+  constexpr int kBlock = block_for<MODE>();
+  auto kern = k_resident<TI, TG, MODE, K, NV, kBlock>;
   const DevInfo di = device_info();
   if (!di.coop || di.cus == 0) return hipSuccess;
   const int ng = a.V / E;
@@ -657,7 +672,7 @@ hipError_t launch_k(const LossArgs& a, bool* used) {
   p.slots = reinterpret_cast<uint64_t*>(a.ws.resident);
   p.err = reinterpret_cast<unsigned*>(p.slots + words(T));
   const int64_t nclear = words(T) + 1;
-  k_clear<<<64, kBlock, 0, a.stream>>>(p.slots, nclear);
+  k_clear<<<64, kClearBlock, 0, a.stream>>>(p.slots, nclear);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   void* args[] = {&p};
   e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(unsigned(T * W)), dim3(kBlock), args, 0,
