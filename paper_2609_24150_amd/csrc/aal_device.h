@@ -221,12 +221,23 @@ static __device__ __forceinline__ void wave_lse_n(float (&msc)[N], float (&s)[N]
   wave_sum_n(s);
 }
 
-// Integer min and fp64 sums are needed once per row only: a butterfly through
-// __shfl_xor is enough there.
-static __device__ __forceinline__ int wave_min_i(int v) {
-  for (int off = 32; off > 0; off >>= 1) v = min(v, __shfl_xor(v, off, 64));
-  return v;
+// Integer minimum over the wave (DPP steps as above), broadcast to all lanes.
+template <int Ctrl, int RowMask = 0xF>
+static __device__ __forceinline__ int dppi(int v, int id) {
+  return __builtin_amdgcn_update_dpp(id, v, Ctrl, RowMask, 0xF, false);
 }
+static __device__ __forceinline__ int wave_min_i(int v) {
+  v = min(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true));
+  v = min(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true));
+  v = min(v, __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, true));
+  v = min(v, __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, true));
+  v = min(v, dppi<0x142, 0xA>(v, INT_MAX));
+  v = min(v, dppi<0x143, 0xC>(v, INT_MAX));
+  return __builtin_amdgcn_readlane(v, 63);
+}
+
+// fp64 sums are needed once per row only: a butterfly through __shfl_xor is
+// enough there.
 
 static __device__ __forceinline__ double wave_sum_d(double v) {
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);

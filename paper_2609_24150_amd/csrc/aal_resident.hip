@@ -63,7 +63,7 @@ struct ResParams {
   float* window_e;
   float* accept;
   int32_t* xstar;
-  uint64_t* slots;     // [parity 2][phase 2][T][K][W][4] words {value bits, tag}
+  uint64_t* slots;     // [parity 2][T][K][W][8] words {value bits, tag}: 0-4 phase A, 4-5 phase B
   unsigned* err;       // [1]
 };
 
@@ -88,6 +88,21 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
 __device__ __forceinline__ u32x4 bld16(rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kNontemporal);
 }
+// The same 16 bytes per lane, delivered straight to LDS: lane l of the wave
+// writes bytes [16 l, 16 l + 16) from `dst` (wave-uniform), no VGPRs involved.
+typedef __attribute__((address_space(3))) void lds_void_t;
+__device__ __forceinline__ void bld16_lds(rsrc_t r, void* dst, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)dst, 16, voff, soff, 0, kNontemporal);
+}
+// s_waitcnt vmcnt(0) as an instruction the compiler's wait-count tracking sees
+// (gfx9 encoding: vmcnt 0, expcnt 7, lgkmcnt 15).
+__device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// Workgroup barrier for LDS data only.  __syncthreads() is also a release
+// fence for every LDS write, which includes staging loads still in flight, so
+// it would wait for them; the workgroup exchanges in this kernel go through
+// ordinary LDS stores (and global atomics that carry their own tags), so
+// draining the LDS queue is all a barrier needs.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // One vector of gradient values at per-lane byte offset `off` of a row.
 template <class TG, int E>
@@ -174,12 +189,27 @@ __device__ __forceinline__ void lse_fold(float& m, float& acc, float msc, float 
     m = nm;
   }
 }
-// Merge (value, index) keeping the larger value, then the lower index.
-__device__ __forceinline__ void argmax_fold(float& bv, float& bi, float v, float i) {
+// Merge (value, index, payload) keeping the larger value, then the lower
+// index; the payload (the draft logit at that index) travels with it.
+__device__ __forceinline__ void argmax_fold(float& bv, float& bi, float& bz, float v, float i, float z) {
   if (v > bv || (v == bv && __builtin_bit_cast(int, i) < __builtin_bit_cast(int, bi))) {
     bv = v;
     bi = i;
+    bz = z;
   }
+}
+
+// Wave-wide argmax of (value, index) pairs, lowest index on ties, with the
+// payload of the winning lane.  All lanes receive the result.
+__device__ __forceinline__ void wave_argmax(float& bv, float& bi, float& bz) {
+  float m[1] = {bv};
+  wave_max_n(m);
+  const int x = wave_min_i(bv == m[0] ? __builtin_bit_cast(int, bi) : INT_MAX);
+  const uint64_t own = __builtin_amdgcn_ballot_w64(bv == m[0] && __builtin_bit_cast(int, bi) == x);
+  const int src = own != 0 ? __builtin_ctzll(own) : 0;
+  bz = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bz), src));
+  bv = m[0];
+  bi = __builtin_bit_cast(float, x);
 }
 
 template <class TI, class TG, int MODE, int K, int NV, int kBlock>
@@ -188,8 +218,20 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
   constexpr int E = TI::kVec;
   constexpr bool kWtv = MODE == int(Mode::kWtv);
   constexpr int GS = sizeof(typename TG::storage);  // gradient element bytes
-  static_assert(4 * K <= kWave, "one publishing lane per row component");
-  __shared__ float sh_w[kWaves][K][4];  // per-wave partials
+  // Phase-A components per row: draft (max, sum), target (max, sum) for WTV;
+  // draft (max, sum), target (max, argmax), draft logit at the argmax for EAL.
+  constexpr int kC = kWtv ? 4 : 5;
+  static_assert(kC * K <= kBlock, "one publishing thread per row component");
+  // LDS staging of the team's next window: the first kPre (row, vector) pairs
+  // of both tensors are fetched into LDS at the start of a window and copied
+  // to the registers in phase C, so most of the refill traffic overlaps the
+  // compute phases instead of all of it queueing behind phase C.
+  constexpr int kPairs = K * NV;
+  constexpr int kLdsStage = kBlock >= 512 ? 144 * 1024 : 72 * 1024;  // one or two workgroups per CU
+  constexpr int kPre = kPairs < kLdsStage / (2 * kBlock * 16) ? kPairs : kLdsStage / (2 * kBlock * 16);
+  static_assert(kPre >= 1, "staging holds at least one pair");
+  __shared__ u32x4 sh_pre[kPre][2][kBlock];
+  __shared__ float sh_w[kWaves][K][kC];  // per-wave partials
   __shared__ float sh_row[K][4];        // merged row constants
   __shared__ float sh_coef[K][2];       // gradient coefficients
   __shared__ int sh_x[K];
@@ -216,23 +258,13 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     coff[v] = uint32_t(min(col[v], p.ng - 1)) * 16u;
   }
   const int64_t stride_w = int64_t(K) * p.row_bytes;
-  uint64_t* const slots_team = p.slots + (int64_t(team) * K * p.W) * 4;
-  const int64_t slot_phase = int64_t(p.T) * K * p.W * 4;  // words per (parity, phase) plane
+  // Tagged slots: 8 words per (row, member), one 64-byte line; planes by parity.
+  uint64_t* const slots_team = p.slots + (int64_t(team) * K * p.W) * 8;
+  const int64_t slot_plane = int64_t(p.T) * K * p.W * 8;
 
   u32x4 rd[K][NV], rt[K][NV];
 
   const uint32_t win_bytes = uint32_t(stride_w);
-  auto load_window = [&](int64_t w) {
-    const rsrc_t bd = make_rsrc(p.zd + w * stride_w, win_bytes);
-    const rsrc_t bt = make_rsrc(p.zt + w * stride_w, win_bytes);
-#pragma unroll
-    for (int k = 0; k < K; ++k)
-#pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        rd[k][v] = bld16(bd, coff[v], k * p.row_bytes);
-        rt[k][v] = bld16(bt, coff[v], k * p.row_bytes);
-      }
-  };
   auto pin_all = [&]() {
 #pragma unroll
     for (int k = 0; k < K; ++k)
@@ -244,13 +276,50 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
   };
 
   int64_t w = team;
-  if (w < p.N) load_window(w);
+  if (w < p.N) {
+    // The first window arrives the way later windows do (staged pairs through
+    // LDS, the rest straight to registers), so the loop sees one wait pattern.
+    const rsrc_t bd = make_rsrc(p.zd + w * stride_w, win_bytes);
+    const rsrc_t bt = make_rsrc(p.zt + w * stride_w, win_bytes);
+    const int wbase = __builtin_amdgcn_readfirstlane(wv * kWave);
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int k = i / NV, v = i % NV;
+      bld16_lds(bd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
+      bld16_lds(bt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+    }
+#pragma unroll
+    for (int i = kPre; i < kPairs; ++i) {
+      const int k = i / NV, v = i % NV;
+      rd[k][v] = bld16(bd, coff[v], k * p.row_bytes);
+      rt[k][v] = bld16(bt, coff[v], k * p.row_bytes);
+    }
+    wait_vmem_all();
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int k = i / NV, v = i % NV;
+      rd[k][v] = sh_pre[i][0][tid];
+      rt[k][v] = sh_pre[i][1][tid];
+    }
+    __syncthreads();  // staging is read before the loop restages it
+  }
   uint32_t iter = 0;
   for (; w < p.N; w += p.T, ++iter) {
     const int parity = iter & 1;
     const uint32_t tagA = 2u * (iter + 1u), tagB = tagA + 1u;
-    uint64_t* const slotsA = slots_team + (2 * parity + 0) * slot_phase;
-    uint64_t* const slotsB = slots_team + (2 * parity + 1) * slot_phase;
+    uint64_t* const slots = slots_team + parity * slot_plane;
+
+    const int64_t wn = w + p.T;
+    const bool more = wn < p.N;
+    // Past the team's last window the next-window resources are empty: the
+    // staging and refill loads still issue (so every iteration has the same
+    // memory-counter pattern) but read nothing.
+    const rsrc_t nd = make_rsrc(p.zd + (more ? wn : w) * stride_w, more ? win_bytes : 0u);
+    const rsrc_t nt = make_rsrc(p.zt + (more ? wn : w) * stride_w, more ? win_bytes : 0u);
+    // The first kPre pairs of the next window are staged row by row during
+    // phase A (LDS is free after the end-of-window barrier): issued between
+    // the rows' arithmetic, the staging loads do not stall the wave.
+    const int wbase = __builtin_amdgcn_readfirstlane(wv * kWave);
 
     // ------------------------------------------------------------ phase A
     pin_all();
@@ -264,9 +333,17 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
             rt[k][v] = neg_inf_vec(TI{});
           }
     }
-    float m0[K], s0[K], m1[K], s1[K];
+    float m0[K], s0[K], m1[K], s1[K], z1[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int i = k * NV + v;
+        if (i < kPre) {
+          bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
+          bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+        }
+      }
       float xs[NV][E];
 #pragma unroll
       for (int v = 0; v < NV; ++v) unpackv<TI, E>(rd[k][v], xs[v]);
@@ -304,35 +381,32 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         m1[k] = mt == kNegInf ? kNegInf : mtsc;
         s1[k] = st;
       } else {
-        float best = kNegInf;
+        float best = kNegInf, bz = kNegInf;
         int bidx = INT_MAX;
 #pragma unroll
-        for (int v = 0; v < NV; ++v)
+        for (int v = 0; v < NV; ++v) {
+          float xd[E];  // the draft logits again, for the payload (not kept from above)
+          pin(rd[k][v]);
+          unpackv<TI, E>(rd[k][v], xd);
 #pragma unroll
           for (int e = 0; e < E; ++e)
             if (xs[v][e] > best) {
               best = xs[v][e];
               bidx = col[v] * E + e;
+              bz = xd[e];
             }
+        }
+        // reduced over the wave right away: the results are wave-uniform, so
+        // the per-lane payloads are short-lived
+        float bi = __builtin_bit_cast(float, bidx);
+        wave_argmax(best, bi, bz);
         m1[k] = best;
-        s1[k] = __builtin_bit_cast(float, bidx);
+        s1[k] = bi;
+        z1[k] = bz;
       }
     }
     wave_lse_n(m0, s0);
-    if constexpr (kWtv) {
-      wave_lse_n(m1, s1);
-    } else {
-      float bv[K];
-#pragma unroll
-      for (int k = 0; k < K; ++k) bv[k] = m1[k];
-      wave_max_n(bv);
-#pragma unroll
-      for (int k = 0; k < K; ++k) {
-        const int bi = (m1[k] == bv[k]) ? __builtin_bit_cast(int, s1[k]) : INT_MAX;
-        s1[k] = __builtin_bit_cast(float, wave_min_i(bi));
-        m1[k] = bv[k];
-      }
-    }
+    if constexpr (kWtv) wave_lse_n(m1, s1);
     if (lane == 0) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
@@ -340,23 +414,25 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         sh_w[wv][k][1] = s0[k];
         sh_w[wv][k][2] = m1[k];
         sh_w[wv][k][3] = s1[k];
+        if constexpr (!kWtv) sh_w[wv][k][4] = z1[k];
       }
     }
-    __syncthreads();
-    if (tid < 4 * K) {  // merge the 4 waves (fixed order), publish one component each
-      const int k = tid >> 2, c = tid & 3;
+    lds_barrier();
+    if (tid < kC * K) {  // merge the waves (fixed order), publish one component each
+      const int k = tid / kC, c = tid % kC;
       float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
+      float a4 = kWtv ? 0.f : sh_w[0][k][kC - 1];
 #pragma unroll
       for (int i = 1; i < kWaves; ++i) {
         lse_fold(a0, a1, sh_w[i][k][0], sh_w[i][k][1]);
         if constexpr (kWtv) {
           lse_fold(a2, a3, sh_w[i][k][2], sh_w[i][k][3]);
         } else {
-          argmax_fold(a2, a3, sh_w[i][k][2], sh_w[i][k][3]);
+          argmax_fold(a2, a3, a4, sh_w[i][k][2], sh_w[i][k][3], sh_w[i][k][kC - 1]);
         }
       }
-      const float val = c == 0 ? a0 : c == 1 ? a1 : c == 2 ? a2 : a3;
-      publish(slotsA + (int64_t(k) * p.W + member) * 4 + c, val, tagA);
+      const float val = c == 0 ? a0 : c == 1 ? a1 : c == 2 ? a2 : c == 3 ? a3 : a4;
+      publish(slots + (int64_t(k) * p.W + member) * 8 + c, val, tagA);
     }
 
     // ------------------------------------------------------------ phase B
@@ -364,16 +440,16 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     // j+64, ... in order, then a fixed DPP tree: every member of the team
     // obtains bit-identical row constants.
     for (int k = wv; k < K; k += kWaves) {
-      float a0[1] = {kNegInf}, a1[1] = {0.f}, a2[1] = {kNegInf}, a3[1];
+      float a0[1] = {kNegInf}, a1[1] = {0.f}, a2[1] = {kNegInf}, a3[1], a4 = kNegInf;
       a3[0] = kWtv ? 0.f : __builtin_bit_cast(float, INT_MAX);
       for (int j = lane; j < p.W; j += kWave) {
-        float q[4];
-        collect<4>(slotsA + (int64_t(k) * p.W + j) * 4, tagA, p.err, q);
+        float q[kC];
+        collect<kC>(slots + (int64_t(k) * p.W + j) * 8, tagA, p.err, q);
         lse_fold(a0[0], a1[0], q[0], q[1]);
         if constexpr (kWtv) {
           lse_fold(a2[0], a3[0], q[2], q[3]);
         } else {
-          argmax_fold(a2[0], a3[0], q[2], q[3]);
+          argmax_fold(a2[0], a3[0], a4, q[2], q[3], q[kC - 1]);
         }
       }
       wave_lse_n(a0, a1);
@@ -386,13 +462,15 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           sh_row[k][3] = __log2f(a3[0]);
         }
       } else {
-        float bv[1] = {a2[0]};
-        wave_max_n(bv);
-        int x = wave_min_i(a2[0] == bv[0] ? __builtin_bit_cast(int, a3[0]) : INT_MAX);
+        wave_argmax(a2[0], a3[0], a4);
+        int x = __builtin_bit_cast(int, a3[0]);
         if (lane == 0) {
-          if (x == INT_MAX) x = 0;  // no finite target logit: unspecified, stay in bounds
+          float zx = a4;  // the draft logit at x, carried through the merges
+          if (x == INT_MAX) {  // no finite target logit: unspecified, stay in bounds
+            x = 0;
+            zx = TI::load1(p.zd + (w * K + k) * int64_t(p.row_bytes), 0);
+          }
           const float l2s = __log2f(a1[0]);
-          const float zx = TI::load1(p.zd + (w * K + k) * int64_t(p.row_bytes), x);
           sh_x[k] = x;
           sh_row[k][0] = a0[0];
           sh_row[k][1] = l2s;
@@ -400,7 +478,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         }
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     if constexpr (kWtv) {
       pin_all();
@@ -440,19 +518,19 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           sh_w[wv][k][1] = aq[k];
         }
       }
-      __syncthreads();
+      lds_barrier();
       if (tid < 2 * K) {
         const int k = tid >> 1, c = tid & 1;
         float r = sh_w[0][k][c];
 #pragma unroll
         for (int i = 1; i < kWaves; ++i) r += sh_w[i][k][c];
-        publish(slotsB + (int64_t(k) * p.W + member) * 4 + c, r * ex2(-sh_row[k][1]), tagB);
+        publish(slots + (int64_t(k) * p.W + member) * 8 + 4 + c, r * ex2(-sh_row[k][1]), tagB);
       }
       for (int k = wv; k < K; k += kWaves) {
         float r[2] = {0.f, 0.f};
         for (int j = lane; j < p.W; j += kWave) {
           float q[2];
-          collect<2>(slotsB + (int64_t(k) * p.W + j) * 4, tagB, p.err, q);
+          collect<2>(slots + (int64_t(k) * p.W + j) * 8 + 4, tagB, p.err, q);
           r[0] += q[0];
           r[1] += q[1];
         }
@@ -462,7 +540,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           sh_coef[k][1] = r[1];  // Q<_k
         }
       }
-      __syncthreads();
+      lds_barrier();
     }
 
     // --------------------------------------------------------------- scan
@@ -508,19 +586,22 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         }
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ------------------------------------------------------------ phase C
-    // Gradient from the registers; each slot is refilled with the team's next
-    // window right after its gradient is stored.
-    const int64_t wn = w + p.T;
-    const bool more = wn < p.N;
-    const rsrc_t nd = make_rsrc(p.zd + (more ? wn : w) * stride_w, win_bytes);
-    const rsrc_t nt = make_rsrc(p.zt + (more ? wn : w) * stride_w, win_bytes);
+    // Gradient from the registers; each pair of slots is refilled with the
+    // team's next window right after its gradient is stored: the unstaged
+    // pairs first from HBM (the longest time to land), then the staged pairs
+    // from LDS.
+    // without a gradient output the stores go to an empty resource (dropped)
     uint8_t* const gw = p.grad ? p.grad + w * int64_t(K) * p.grow_bytes : nullptr;
+    const uint32_t grow = gw != nullptr ? p.grow_bytes : 0u;
+    wait_vmem_all();  // staging has landed (issued a whole phase A and B earlier)
     pin_all();
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
+    for (int j = 0; j < kPairs; ++j) {
+      const int i = (j + kPre) % kPairs;
+      const int k = i / NV, v = i % NV;
       // q = 2^-l2sd 2^u: the row factor 2^-l2sd is folded into the coefficients
       const float mscd = sh_row[k][0], rs = ex2(-sh_row[k][1]);
       float msct = 0.f, dl = 0.f, cA, cB = 0.f;
@@ -535,34 +616,31 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       } else {
         cA = -sh_coef[k][0] * rs;
       }
-      uint8_t* const gk = gw + k * p.grow_bytes;
-      const rsrc_t gr = make_rsrc(gk, p.grow_bytes);  // slots past the row end are dropped
+      const rsrc_t gr = make_rsrc(gw + k * grow, grow);  // slots past the row end are dropped
+      float xd[E], g[E];
+      unpackv<TI, E>(rd[k][v], xd);
+      if constexpr (kWtv) {
+        float xt[E];
+        unpackv<TI, E>(rt[k][v], xt);
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        if (gw != nullptr) {
-          float xd[E], g[E];
-          unpackv<TI, E>(rd[k][v], xd);
-          if constexpr (kWtv) {
-            float xt[E];
-            unpackv<TI, E>(rt[k][v], xt);
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-              const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
-              const float t = __builtin_fmaf(xt[e], p.sct, -msct) - dl;
-              g[e] = ex2(u) * ((u < t) ? cA : cB);
-            }
-          } else {
-            // -c q everywhere; the greedy token's entry is fixed up after the loop
-#pragma unroll
-            for (int e = 0; e < E; ++e) g[e] = cA * ex2(__builtin_fmaf(xd[e], p.scd, -mscd));
-          }
-          store_g<TG, E>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
+        for (int e = 0; e < E; ++e) {
+          const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
+          const float t = __builtin_fmaf(xt[e], p.sct, -msct) - dl;
+          g[e] = ex2(u) * ((u < t) ? cA : cB);
         }
-        asm volatile("" ::: "memory");  // keep the refill below this slot's store
-        if (more) {
-          rd[k][v] = bld16(nd, coff[v], k * p.row_bytes);
-          rt[k][v] = bld16(nt, coff[v], k * p.row_bytes);
-        }
+      } else {
+        // -c q everywhere; the greedy token's entry is fixed up after the loop
+#pragma unroll
+        for (int e = 0; e < E; ++e) g[e] = cA * ex2(__builtin_fmaf(xd[e], p.scd, -mscd));
+      }
+      store_g<TG, E>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
+      asm volatile("" ::: "memory");  // keep the refill below this slot's store
+      if (i < kPre) {
+        rd[k][v] = sh_pre[i][0][tid];
+        rt[k][v] = sh_pre[i][1][tid];
+      } else {
+        rd[k][v] = bld16(nd, coff[v], k * p.row_bytes);
+        rt[k][v] = bld16(nt, coff[v], k * p.row_bytes);
       }
     }
     if constexpr (!kWtv) {
@@ -582,8 +660,9 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         }
       }
     }
-    __syncthreads();  // sh_row / sh_coef are rewritten by the next window
+    lds_barrier();  // sh_row / sh_coef and the staging are rewritten by the next window
   }
+  wait_vmem_all();  // the last (empty) staging loads retire before the workgroup ends
 }
 
 // Marks the loss NaN if any poll timed out.
@@ -619,12 +698,18 @@ DevInfo device_info() {
   return cache[dev];
 }
 
-// Workgroup size per mode: WTV synchronises a team twice per window, so fewer,
-// wider members (512 threads, one workgroup per CU) pay less team skew; EAL
-// synchronises once and gains more from a second co-resident workgroup per CU.
+// Workgroup size per mode: one 512-thread workgroup per CU, which keeps the
+// teams small (less skew at each team synchronisation) and gives the LDS
+// staging the whole 144 KiB.
+#ifndef AAL_WTV_BLOCK
+#define AAL_WTV_BLOCK 512
+#endif
+#ifndef AAL_EAL_BLOCK
+#define AAL_EAL_BLOCK 512
+#endif
 template <int MODE>
 constexpr int block_for() {
-  return MODE == int(Mode::kWtv) ? 512 : 256;
+  return MODE == int(Mode::kWtv) ? AAL_WTV_BLOCK : AAL_EAL_BLOCK;
 }
 
 template <class TI, class TG, int MODE, int K>
@@ -649,7 +734,7 @@ hipError_t launch_k(const LossArgs& a, bool* used) {
   if (T >= 8) T -= T % 8;
   if (T > a.N) T = a.N;
   if (T < 1) return hipSuccess;  // a window does not fit: streaming schedule
-  auto words = [&](int64_t t) { return int64_t(2) * 2 * t * K * W * 4; };
+  auto words = [&](int64_t t) { return int64_t(2) * t * K * W * 8; };
   while (T > 8 && size_t(words(T) + 1) * 8 > a.ws.resident_bytes) T -= 8;
   if (size_t(words(T) + 1) * 8 > a.ws.resident_bytes) return hipSuccess;
   ResParams p{};
