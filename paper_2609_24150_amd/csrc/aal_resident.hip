@@ -483,14 +483,14 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     if constexpr (kWtv) {
       pin_all();
       float am[K], aq[K];
-      // With u, w the two fmas below, log2 q = u - l2sd and log2 p = w - l2st,
-      // so min(p, q) = 2^-l2sd 2^min(u, w - dl) and [q < p] = [u < w - dl] for
-      // dl = l2st - l2sd: the common factor is applied once per row after the
-      // reductions.
+      // With u = x_d sc_d - msc_d and t = x_t sc_t - (msc_t + dl), each one
+      // fma, log2 q = u - l2sd and log2 p = t - l2sd for dl = l2st - l2sd, so
+      // min(p, q) = 2^-l2sd 2^min(u, t) and [q < p] = [u < t]: the common
+      // factor is applied once per row after the reductions.
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         const float mscd = sh_row[k][0];
-        const float msct = sh_row[k][2], dl = sh_row[k][3] - sh_row[k][1];
+        const float ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
         float sm = 0.f, sq = 0.f;
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
@@ -500,7 +500,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
           for (int e = 0; e < E; ++e) {
             const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
-            const float t = __builtin_fmaf(xt[e], p.sct, -msct) - dl;
+            const float t = __builtin_fmaf(xt[e], p.sct, -ct);
             const float mn = ex2(fminf(u, t));
             sm += mn;
             sq += (u < t) ? mn : 0.f;
@@ -604,10 +604,9 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       const int k = i / NV, v = i % NV;
       // q = 2^-l2sd 2^u: the row factor 2^-l2sd is folded into the coefficients
       const float mscd = sh_row[k][0], rs = ex2(-sh_row[k][1]);
-      float msct = 0.f, dl = 0.f, cA, cB = 0.f;
+      float ct = 0.f, cA, cB = 0.f;
       if constexpr (kWtv) {
-        msct = sh_row[k][2];
-        dl = sh_row[k][3] - sh_row[k][1];
+        ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);  // as in phase B
         cA = sh_coef[k][0] * rs;
         cB = sh_coef[k][1] * rs;
         // keep the products: the select below would otherwise absorb them and
@@ -625,7 +624,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
-          const float t = __builtin_fmaf(xt[e], p.sct, -msct) - dl;
+          const float t = __builtin_fmaf(xt[e], p.sct, -ct);
           g[e] = ex2(u) * ((u < t) ? cA : cB);
         }
       } else {
