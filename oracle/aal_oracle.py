@@ -50,6 +50,12 @@ __all__ = [
     "sim_accept_grpo",
     "sim_near_threshold",
     "wtv_near_ties",
+    "LAYOUT_WINDOWS",
+    "LAYOUT_SEQUENCES",
+    "window_rows",
+    "forward_kl",
+    "window_length_coefficients",
+    "combined_loss",
 ]
 
 
@@ -280,6 +286,121 @@ def sim_accept_grpo(z_draft, z_target, T: float, u1, u2, eps: float = 1e-6,
     x, acc, r, _, _ = simulate_acceptance(z_draft, z_target, T, u1, u2)
     return {"token": x, "accept": acc, "reward": r,
             "advantage": group_advantage(r, eps, ddof, clip)}
+
+
+# ---------------------------------------------------------------------------
+# Sliding windows over sequences and the combined objectives of the
+# experiments (Section "Window TV Loss", Figure wtv; Section "Settings")
+# ---------------------------------------------------------------------------
+LAYOUT_WINDOWS = 0    # [N, K, V]: N disjoint windows of K positions
+LAYOUT_SEQUENCES = 1  # [B, S, V]: B sequences; a window starts at every t <= S - K
+
+
+def window_rows(layout: int, B: int, S: int, K: int) -> np.ndarray:
+    """Row indices [W, K] of every window.
+
+    Windows layout: window n covers rows n*K .. n*K+K-1 (S is ignored).
+    Sequences layout: the draft and the target are run once over each
+    sequence and a window of K positions starts at every position t of it
+    (the windows slide by one); only windows that fit entirely in the
+    sequence are counted, so sequence b contributes windows t = 0..S-K,
+    covering rows b*S + t .. b*S + t + K - 1.
+    """
+    if layout == LAYOUT_WINDOWS:
+        return np.arange(B * K, dtype=np.int64).reshape(B, K)
+    if layout == LAYOUT_SEQUENCES:
+        if S < K:
+            return np.zeros((0, K), np.int64)
+        starts = (np.arange(B)[:, None] * S + np.arange(S - K + 1)[None, :]).reshape(-1)
+        return starts[:, None] + np.arange(K)[None, :]
+    raise ValueError("unknown layout")
+
+
+def forward_kl(z_draft, z_target, T_draft: float, T_target: float):
+    """Per-position forward KL of the anchor loss: KL(p~ || q~) =
+    sum_v p~(v) (log p~(v) - log q~(v)), target p~ against draft q~, both at
+    their temperatures (Section "Settings").  Returns (kl, q, p)."""
+    lq = tempered_log_softmax(z_draft, T_draft)
+    lp = tempered_log_softmax(z_target, T_target)
+    p = np.exp(lp)
+    return np.sum(p * (lp - lq), axis=-1), np.exp(lq), p
+
+
+def window_length_coefficients(a, windows: np.ndarray):
+    """For per-row acceptances ``a`` [R] and window rows [W, K]: the expected
+    lengths E_w = sum_k prod_{j<k} a_{w,j} (Eq. eal_generic) and, per row,
+    sum over the windows that contain it of dE_w/da_row."""
+    a = np.asarray(a, np.float64)
+    A = a[windows]
+    E = expected_length(A) if len(windows) else np.zeros(0)
+    dE = expected_length_grad(A) if len(windows) else np.zeros((0, windows.shape[1]))
+    per_row = np.zeros_like(a)
+    np.add.at(per_row, windows.reshape(-1), dE.reshape(-1))
+    return E, per_row
+
+
+def combined_loss(z_draft, z_target, T_draft: float, T_target: float, weights, layout: int,
+                  B: int, S: int, K: int, labels=None, grad_scale: float = 1.0):
+    """A weighted sum of the paper's training objectives over one batch:
+
+        loss = w_wtv L_WTV + w_eal L_EAL + w_kl L_KL + w_tv L_TV
+
+    * L_WTV = -(1/W) sum_windows E[L] with a = 1 - TV (Eq. loss_tv);
+    * L_EAL = -(1/W) sum_windows E[L] with a = q~(x*) (Eq. loss_eal), x* the
+      given label of the position, else the target's greedy token;
+    * L_KL  = (1/R) sum_positions KL(p~ || q~), the forward-KL anchor;
+    * L_TV  = (1/W) sum_windows (1/K) sum_j TV(p~, q~), the per-window mean
+      TV auxiliary of the baselines (Section "Settings").
+    W is the number of windows (``window_rows``), R the number of positions.
+    Logits are [R, V] rows (any leading shape is flattened).  The gradient
+    w.r.t. the draft logits chains each term through the softmax Jacobian at
+    T_draft (the target is frozen): d a_tv / d z = (1/T) q (m - Q<),
+    d a_eal / d z = (1/T) a (1[v=x*] - q), d KL / d z = (1/T) (q - p).
+
+    Returns a dict: loss, terms [4] (L_WTV, L_EAL, L_KL, L_TV), E_tv [W],
+    E_eal [W], a_tv [R], qlt [R], a_eal [R], xstar [R], kl [R], grad [R, V].
+    """
+    zd = np.asarray(z_draft, np.float64)
+    zt = np.asarray(z_target, np.float64)
+    V = zd.shape[-1]
+    zd = zd.reshape(-1, V)
+    zt = zt.reshape(-1, V)
+    R = zd.shape[0]
+    w_wtv, w_eal, w_kl, w_tv = (float(x) for x in weights)
+    win = window_rows(layout, B, S, K)
+    W = len(win)
+
+    a_tv, q, p = acceptance_sampling(zd, zt, T_draft, T_target)
+    m = (q < p).astype(np.float64)
+    qlt = np.sum(m * q, axis=-1)
+    xs = greedy_token(zt) if labels is None else np.asarray(labels, np.int64).reshape(-1)
+    a_eal = np.take_along_axis(q, xs[:, None], axis=-1)[:, 0]
+    kl, _, _ = forward_kl(zd, zt, T_draft, T_target)
+
+    E_tv, dEtv = window_length_coefficients(a_tv, win)
+    E_eal, dEeal = window_length_coefficients(a_eal, win)
+    count = np.zeros(R)
+    np.add.at(count, win.reshape(-1), 1.0)  # windows that contain each row
+
+    terms = np.array([
+        -np.sum(E_tv) / W if W else 0.0,
+        -np.sum(E_eal) / W if W else 0.0,
+        np.sum(kl) / R,
+        np.sum(count * (1.0 - a_tv)) / (W * K) if W else 0.0,
+    ])
+    loss = w_wtv * terms[0] + w_eal * terms[1] + w_kl * terms[2] + w_tv * terms[3]
+
+    # dloss/da per row, then through the softmax Jacobians
+    g_tv = (-w_wtv * dEtv - w_tv * count / K) / W if W else np.zeros(R)
+    g_eal = -w_eal * dEeal / W if W else np.zeros(R)
+    g_kl = np.full(R, w_kl / R)
+    onehot = np.zeros_like(q)
+    np.put_along_axis(onehot, xs[:, None], 1.0, axis=-1)
+    grad = (g_tv[:, None] * q * (m - qlt[:, None])
+            + (g_eal * a_eal)[:, None] * (onehot - q)
+            + g_kl[:, None] * (q - p)) * (grad_scale / T_draft)
+    return {"loss": loss, "terms": terms, "E_tv": E_tv, "E_eal": E_eal, "a_tv": a_tv,
+            "qlt": qlt, "a_eal": a_eal, "xstar": xs, "kl": kl, "grad": grad}
 
 
 # ---------------------------------------------------------------------------
