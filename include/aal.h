@@ -162,6 +162,73 @@ aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_
                                  float eps, int32_t std_ddof, float adv_clip,
                                  void* workspace, size_t workspace_bytes, void* stream);
 
+/* Row layouts of the combined-objective entry point. */
+typedef enum {
+  AAL_LAYOUT_WINDOWS = 0,  /* [B,K,V]: B disjoint windows of K positions                */
+  AAL_LAYOUT_SEQUENCES = 1 /* [B,S,V]: B sequences of S positions; a window of K positions
+                              starts at every t = 0..S-K (windows slide by one)          */
+} aal_layout_t;
+
+/* Weights of the terms of the combined objective (any may be 0). */
+typedef struct {
+  float wtv; /* L_WTV: -(1/W) sum_windows E[L], a = 1 - TV                                */
+  float eal; /* L_EAL: -(1/W) sum_windows E[L], a = q(x*)                                 */
+  float kl;  /* L_KL : (1/R) sum_positions KL(p || q), the forward-KL anchor              */
+  float tv;  /* L_TV : (1/W) sum_windows (1/K) sum_{j<K} TV(p, q), the window-mean TV     */
+} aal_loss_weights_t;
+
+/* Workspace bytes of aal_loss_fwd_bwd for the given layout and sizes (0 for
+ * invalid arguments). */
+size_t aal_loss_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32_t K);
+
+/*
+ * Combined training objective, forward and backward: the paper's sliding
+ * windows over sequences (Section "Window TV Loss", Figure wtv: one draft and
+ * one target pass give a_t for every position, each window reads
+ * a_t..a_{t+K-1}) and the objectives of its experiments (Section "Settings":
+ * the forward-KL anchor alone or plus 0.1 L_EAL, plus the window-mean TV, and
+ * L_WTV alone).
+ *
+ *   q = softmax(z_draft / temp_draft), p = softmax(z_target / temp_target), per row
+ *   a_tv = sum_v min(p, q);   a_eal = q(x*), x* = labels[r] if labels, else
+ *                             argmax_v z_target (lowest index on ties)
+ *   KL_r = sum_v p (log p - log q)
+ *   loss = wtv L_WTV + eal L_EAL + kl L_KL + tv L_TV   (see aal_loss_weights_t)
+ *   E over a window of rows r_0..r_{K-1}: sum_{k=1..K} prod_{j<k} a_{r_j}
+ *   grad_draft = scale * dloss/dz_draft, with
+ *     d a_tv/dz = q (m - sum_u m(u) q(u)) / temp_draft, m = 1[q < p],
+ *     d a_eal/dz = a_eal (1[v = x*] - q) / temp_draft,
+ *     d KL/dz = (q - p) / temp_draft;
+ *   a row's dloss/da sums over every window that contains it.
+ *
+ * Rows: R = B*K (windows layout; S is ignored) or B*S (sequences layout),
+ * row-major [R, V]; windows: W = B or B*max(0, S-K+1).  With W = 0 the window
+ * terms are 0.
+ * z_draft : [R,V] of in_dtype, required.
+ * z_target: [R,V] of in_dtype; may be NULL only when wtv = kl = tv = 0 and
+ *           labels are given (the EAL term then needs no target).
+ * labels  : [R] int32 token ids in [0, V), or NULL; out-of-range ids are
+ *           clamped into [0, V).
+ * B >= 1, 1 <= K <= 64, V >= 1, S >= 1 (sequences), R*V < 2^62; temperatures
+ * finite and > 0; weights finite.
+ * loss    : [1] float, required.   terms: [4] float (L_WTV, L_EAL, L_KL, L_TV) or NULL;
+ *           a term whose weight is 0 is not evaluated and reads 0.
+ * e_tv, e_eal : [W] float window expectations, or NULL.
+ * accept_tv, accept_eal : [R] float a_tv / a_eal, or NULL.   xstar: [R] int32, or NULL.
+ *           a_tv and e_tv are evaluated when wtv, kl or tv is non-zero; a_eal,
+ *           e_eal and x* when eal is non-zero; otherwise they read 0 (x*: -1).
+ * grad_draft, grad_dtype, grad_scale : as for aal_eal_fwd_bwd.
+ * workspace : at least aal_loss_workspace_bytes(layout, B, S, K) bytes.
+ */
+aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const int32_t* labels,
+                              aal_dtype_t in_dtype, aal_layout_t layout, int64_t B, int32_t S,
+                              int32_t K, int32_t V, float temp_draft, float temp_target,
+                              aal_loss_weights_t weights, float* loss, float* terms,
+                              float* e_tv, float* e_eal, float* accept_tv, float* accept_eal,
+                              int32_t* xstar, void* grad_draft, aal_dtype_t grad_dtype,
+                              const float* grad_scale, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
 #ifdef __cplusplus
 }
 #endif

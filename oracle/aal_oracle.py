@@ -358,7 +358,9 @@ def combined_loss(z_draft, z_target, T_draft: float, T_target: float, weights, l
     d a_eal / d z = (1/T) a (1[v=x*] - q), d KL / d z = (1/T) (q - p).
 
     Returns a dict: loss, terms [4] (L_WTV, L_EAL, L_KL, L_TV), E_tv [W],
-    E_eal [W], a_tv [R], qlt [R], a_eal [R], xstar [R], kl [R], grad [R, V].
+    E_eal [W], a_tv [R], qlt [R], a_eal [R], xstar [R], kl [R], grad [R, V],
+    and the per-row Jacobian coefficients coef_tv, coef_eal, coef_kl [R]
+    (grad = coef_tv q (m - Q<) + coef_eal (1[v=x*] - q) + coef_kl (q - p)).
     """
     zd = np.asarray(z_draft, np.float64)
     zt = np.asarray(z_target, np.float64)
@@ -399,8 +401,10 @@ def combined_loss(z_draft, z_target, T_draft: float, T_target: float, weights, l
     grad = (g_tv[:, None] * q * (m - qlt[:, None])
             + (g_eal * a_eal)[:, None] * (onehot - q)
             + g_kl[:, None] * (q - p)) * (grad_scale / T_draft)
+    f = grad_scale / T_draft
     return {"loss": loss, "terms": terms, "E_tv": E_tv, "E_eal": E_eal, "a_tv": a_tv,
-            "qlt": qlt, "a_eal": a_eal, "xstar": xs, "kl": kl, "grad": grad}
+            "qlt": qlt, "a_eal": a_eal, "xstar": xs, "kl": kl, "grad": grad,
+            "coef_tv": g_tv * f, "coef_eal": g_eal * a_eal * f, "coef_kl": g_kl * f}
 
 
 # ---------------------------------------------------------------------------

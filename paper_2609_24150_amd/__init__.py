@@ -8,7 +8,11 @@ from .api import (  # noqa: F401
     AAL_BF16,
     AAL_F32,
     AAL_FLAG_STREAMING,
+    AAL_LAYOUT_SEQUENCES,
+    AAL_LAYOUT_WINDOWS,
     aal_eal_fwd_bwd,
+    aal_loss_fwd_bwd,
+    aal_loss_workspace_bytes,
     aal_sim_accept_grpo,
     aal_workspace_bytes,
     aal_wtv_fwd_bwd,

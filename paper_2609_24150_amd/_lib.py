@@ -19,6 +19,14 @@ AAL_ERR_ALIGN = 3
 AAL_ERR_WORKSPACE = 4
 AAL_ERR_HIP = 5
 AAL_FLAG_STREAMING = 1
+AAL_LAYOUT_WINDOWS = 0
+AAL_LAYOUT_SEQUENCES = 1
+
+
+class LossWeights(C.Structure):
+    """aal_loss_weights_t (passed by value)."""
+    _fields_ = [("wtv", C.c_float), ("eal", C.c_float), ("kl", C.c_float), ("tv", C.c_float)]
+
 
 _vp = C.c_void_p
 _SIGNATURES = {
@@ -41,6 +49,11 @@ _SIGNATURES = {
         _vp, _vp, _vp, _vp, _vp, _vp,
         C.c_float, C.c_int32, C.c_float,
         _vp, C.c_size_t, _vp]),
+    "aal_loss_workspace_bytes": (C.c_size_t, [C.c_int, C.c_int64, C.c_int32, C.c_int32]),
+    "aal_loss_fwd_bwd": (C.c_int, [
+        _vp, _vp, _vp, C.c_int, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_float, C.c_float,
+        LossWeights, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+        _vp, C.c_int, _vp, _vp, C.c_size_t, _vp]),
 }
 
 _lib = None

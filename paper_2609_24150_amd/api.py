@@ -8,7 +8,7 @@ from __future__ import annotations
 import torch
 
 from . import _lib
-from ._lib import AAL_BF16, AAL_F32, AAL_FLAG_STREAMING  # noqa: F401
+from ._lib import AAL_BF16, AAL_F32, AAL_FLAG_STREAMING, AAL_LAYOUT_SEQUENCES, AAL_LAYOUT_WINDOWS  # noqa: F401
 
 _DT = {torch.bfloat16: AAL_BF16, torch.float32: AAL_F32}
 
@@ -141,4 +141,65 @@ def aal_sim_accept_grpo(z_draft: torch.Tensor, z_target: torch.Tensor, u1: torch
         _ptr(out["advantage"]), float(eps), int(std_ddof), float(adv_clip),
         _ptr(ws), ws.numel(), _stream(dev, stream))
     _lib.check(st, "aal_sim_accept_grpo")
+    return out
+
+
+def aal_loss_workspace_bytes(layout: int, B: int, S: int, K: int) -> int:
+    return int(_lib.lib().aal_loss_workspace_bytes(int(layout), int(B), int(S), int(K)))
+
+
+def aal_loss_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor | None, K: int, *,
+                     weights=(0.0, 0.0, 0.0, 0.0), temp_draft: float = 1.0, temp_target: float = 1.0,
+                     layout: int = AAL_LAYOUT_WINDOWS, labels: torch.Tensor | None = None,
+                     grad: bool = True, grad_dtype: torch.dtype | None = None,
+                     grad_scale: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> dict:
+    """Combined objective forward + backward (weights = (wtv, eal, kl, tv)).
+
+    Windows layout: logits [N, K, V] (N disjoint windows).  Sequences layout:
+    logits [B, S, V]; a window of K positions starts at every t <= S - K.
+    labels: int32 [rows] (or the logits' leading shape) replacing the greedy
+    target token of the EAL term, or None.  z_target may be None only when
+    the EAL term alone is asked for with labels.
+
+    Returns a dict: loss [1], terms [4] (L_WTV, L_EAL, L_KL, L_TV), E_tv [W],
+    E_eal [W], accept_tv [R], accept_eal [R], xstar [R] int32, grad (the
+    logits' shape, or None)."""
+    if z_draft.dim() != 3 or not z_draft.is_cuda or not z_draft.is_contiguous():
+        raise ValueError("z_draft must be a contiguous [B, S or K, V] device tensor")
+    if z_target is not None:
+        if z_target.shape != z_draft.shape or z_target.dtype != z_draft.dtype or not z_target.is_contiguous():
+            raise ValueError("z_target must match z_draft in shape, dtype and layout")
+    B, S, V = z_draft.shape
+    if layout == AAL_LAYOUT_WINDOWS and S != K:
+        raise ValueError("windows layout needs logits of shape [N, K, V]")
+    R = B * S
+    W = B if layout == AAL_LAYOUT_WINDOWS else B * max(0, S - K + 1)
+    dev = z_draft.device
+    if labels is not None and (labels.dtype != torch.int32 or labels.numel() != R or not labels.is_contiguous()
+                               or labels.device != dev):
+        raise ValueError("labels must be a contiguous int32 device tensor with one entry per row")
+    if grad_scale is not None and (grad_scale.dtype != torch.float32 or grad_scale.device != dev):
+        raise TypeError("grad_scale must be a float32 device tensor")
+    out = {
+        "loss": torch.empty(1, dtype=torch.float32, device=dev),
+        "terms": torch.empty(4, dtype=torch.float32, device=dev),
+        "E_tv": torch.empty(W, dtype=torch.float32, device=dev),
+        "E_eal": torch.empty(W, dtype=torch.float32, device=dev),
+        "accept_tv": torch.empty(R, dtype=torch.float32, device=dev),
+        "accept_eal": torch.empty(R, dtype=torch.float32, device=dev),
+        "xstar": torch.empty(R, dtype=torch.int32, device=dev),
+        "grad": torch.empty(B, S, V, dtype=grad_dtype or z_draft.dtype, device=dev) if grad else None,
+    }
+    if ws is None:
+        ws = torch.empty(aal_loss_workspace_bytes(layout, B, S, K), dtype=torch.uint8, device=dev)
+    g = out["grad"]
+    w = _lib.LossWeights(*(float(x) for x in weights))
+    st = _lib.lib().aal_loss_fwd_bwd(
+        _ptr(z_draft), _ptr(z_target), _ptr(labels), _dtype_code(z_draft.dtype), int(layout), B, S, K, V,
+        float(temp_draft), float(temp_target), w, _ptr(out["loss"]), _ptr(out["terms"]),
+        _ptr(out["E_tv"]) if W else None, _ptr(out["E_eal"]) if W else None,
+        _ptr(out["accept_tv"]), _ptr(out["accept_eal"]), _ptr(out["xstar"]),
+        _ptr(g), _dtype_code(g.dtype) if g is not None else AAL_F32, _ptr(grad_scale),
+        _ptr(ws), ws.numel(), _stream(dev, stream))
+    _lib.check(st, "aal_loss_fwd_bwd")
     return out

@@ -244,4 +244,100 @@ aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_
   return AAL_OK;
 }
 
+size_t aal_loss_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32_t K) {
+  if (B < 1 || K < 1 || (layout == AAL_LAYOUT_SEQUENCES && S < 1)) return 0;
+  if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES) return 0;
+  const int64_t rows = layout == AAL_LAYOUT_WINDOWS ? B * K : B * S;
+  const int64_t windows = layout == AAL_LAYOUT_WINDOWS ? B : B * int64_t(S >= K ? S - K + 1 : 0);
+  return aal::general_workspace_bytes(rows, windows);
+}
+
+aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const int32_t* labels, aal_dtype_t in_dtype,
+                              aal_layout_t layout, int64_t B, int32_t S, int32_t K, int32_t V, float temp_draft,
+                              float temp_target, aal_loss_weights_t weights, float* loss, float* terms, float* e_tv,
+                              float* e_eal, float* accept_tv, float* accept_eal, int32_t* xstar, void* grad_draft,
+                              aal_dtype_t grad_dtype, const float* grad_scale, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES)
+    return fail(AAL_ERR_ARG, "unknown layout %d", int(layout));
+  if (B < 1) return fail(AAL_ERR_ARG, "B must be >= 1 (got %lld)", (long long)B);
+  if (K < 1 || K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", K);
+  if (V < 1) return fail(AAL_ERR_ARG, "V must be >= 1 (got %d)", V);
+  if (layout == AAL_LAYOUT_SEQUENCES && S < 1) return fail(AAL_ERR_ARG, "S must be >= 1 (got %d)", S);
+  const int64_t per = layout == AAL_LAYOUT_WINDOWS ? K : S;
+  if (B > ((int64_t(1) << 31) - 1) / per) return fail(AAL_ERR_ARG, "the number of rows must be < 2^31");
+  const int64_t R = B * per;
+  if (R > (int64_t(1) << 62) / V) return fail(AAL_ERR_ARG, "rows*V must be < 2^62");
+  const int64_t W = layout == AAL_LAYOUT_WINDOWS ? B : B * int64_t(S >= K ? S - K + 1 : 0);
+  auto finite = [](float x) {
+    uint32_t u;
+    memcpy(&u, &x, sizeof u);
+    return ((u >> 23) & 0xffu) != 0xffu;
+  };
+  if (!finite(weights.wtv) || !finite(weights.eal) || !finite(weights.kl) || !finite(weights.tv))
+    return fail(AAL_ERR_ARG, "weights must be finite");
+  const bool need_pq = weights.wtv != 0.f || weights.tv != 0.f || weights.kl != 0.f;
+  const bool need_t = need_pq || (weights.eal != 0.f && labels == nullptr);
+  if (!z_draft) return fail(AAL_ERR_ARG, "z_draft must be non-NULL");
+  if (need_t && !z_target)
+    return fail(AAL_ERR_ARG, "z_target must be non-NULL unless only the EAL term is asked for with labels");
+  if (!loss) return fail(AAL_ERR_ARG, "loss must be non-NULL");
+  if (!valid_dtype(int(in_dtype))) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", int(in_dtype));
+  if (grad_draft && !valid_dtype(int(grad_dtype))) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", int(grad_dtype));
+  if (!aligned(z_draft, 16) || (z_target && !aligned(z_target, 16)))
+    return fail(AAL_ERR_ALIGN, "logit pointers must be 16-byte aligned");
+  if (grad_draft && !aligned(grad_draft, 16)) return fail(AAL_ERR_ALIGN, "grad_draft must be 16-byte aligned");
+  const float scd = scale_for(temp_draft);
+  const float sct = scale_for(temp_target);
+  if (!positive_finite(temp_draft) || scd == 0.f)
+    return fail(AAL_ERR_ARG, "temp_draft must be finite, > 0 and >= 1e-37");
+  if (!positive_finite(temp_target) || sct == 0.f)
+    return fail(AAL_ERR_ARG, "temp_target must be finite, > 0 and >= 1e-37");
+  if (!workspace) return fail(AAL_ERR_WORKSPACE, "workspace must be non-NULL");
+  if (!aligned(workspace, 256)) return fail(AAL_ERR_ALIGN, "workspace must be 256-byte aligned");
+  const size_t need = aal::general_workspace_bytes(R, W);
+  if (workspace_bytes < need)
+    return fail(AAL_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+  uint8_t* wp = static_cast<uint8_t*>(workspace);
+  aal::GenArgs a{};
+  a.in = to_dtype(in_dtype);
+  a.gd = to_dtype(grad_dtype);
+  a.zd = z_draft;
+  a.zt = need_t ? z_target : nullptr;
+  a.labels = labels;
+  a.layout = int(layout);
+  a.B = B;
+  a.S = layout == AAL_LAYOUT_WINDOWS ? K : S;
+  a.K = K;
+  a.V = V;
+  a.R = R;
+  a.W = W;
+  a.sc_d = scd;
+  a.sc_t = sct;
+  a.inv_t_d = 1.0f / temp_draft;
+  a.w_wtv = weights.wtv;
+  a.w_eal = weights.eal;
+  a.w_kl = weights.kl;
+  a.w_tv = weights.tv;
+  a.loss = loss;
+  a.terms = terms;
+  a.e_tv = e_tv;
+  a.e_eal = e_eal;
+  a.accept_tv = accept_tv;
+  a.accept_eal = accept_eal;
+  a.xstar = xstar;
+  a.grad = grad_draft;
+  a.grad_scale = grad_scale;
+  a.stats = reinterpret_cast<aal::GenStats*>(wp);
+  wp += aal::align256(size_t(R) * sizeof(aal::GenStats));
+  a.win_tv = reinterpret_cast<float*>(wp);
+  wp += aal::align256(size_t(W) * sizeof(float));
+  a.win_eal = reinterpret_cast<float*>(wp);
+  a.stream = static_cast<hipStream_t>(stream);
+  hipError_t e = aal::launch_general(a);
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
 }  // extern "C"

@@ -89,6 +89,56 @@ hipError_t launch_loss_reduce(const LossArgs& a);
 // wide for the co-resident grid, or no cooperative launch on the device.
 hipError_t launch_resident(const LossArgs& a, bool* used);
 
+// Per-row statistics of the combined-objective schedule.  64 bytes.
+struct GenStats {
+  float msc_d, l2s_d;  // draft: fl(max * sc), log2 of the sum (as RowStats)
+  float msc_t, l2s_t;  // target, when a TV or KL term is asked for
+  float a_tv;          // sum_v min(p, q)
+  float qlt;           // sum of q over entries with q < p
+  float a_eal;         // q(x*)
+  float kl;            // KL(p || q) in nats
+  int32_t xstar;       // greedy target token or label (-1: no EAL term)
+  float cA, cB;        // gradient: q (m ? cA : cB) + cP p + cX 1[v = x*]
+  float cX, cP;
+  float tv_w;          // (windows containing the row) * (1 - a_tv)
+  float pad[2];
+};
+static_assert(sizeof(GenStats) == 64, "GenStats layout");
+
+inline size_t general_workspace_bytes(int64_t rows, int64_t windows) {
+  return align256(size_t(rows) * sizeof(GenStats)) + 2 * align256(size_t(windows) * sizeof(float));
+}
+
+struct GenArgs {
+  DType in;
+  DType gd;
+  const void* zd;
+  const void* zt;          // may be null when no term needs the target
+  const int32_t* labels;   // may be null
+  int layout;              // 0 windows, 1 sequences
+  int64_t B;
+  int S, K, V;
+  int64_t R, W;            // rows, windows
+  float sc_d, sc_t, inv_t_d;
+  float w_wtv, w_eal, w_kl, w_tv;
+  float* loss;
+  float* terms;            // may be null
+  float* e_tv;             // may be null
+  float* e_eal;            // may be null
+  float* accept_tv;        // may be null
+  float* accept_eal;       // may be null
+  int32_t* xstar;          // may be null
+  void* grad;              // may be null
+  const float* grad_scale; // may be null
+  GenStats* stats;         // workspace [R]
+  float* win_tv;           // workspace [W]
+  float* win_eal;          // workspace [W]
+  hipStream_t stream;
+};
+
+// Row pass, window scan, loss, gradient pass.  Handles every shape.
+hipError_t launch_general(const GenArgs& a);
+
 struct SimArgs {
   DType in;
   const void* zd;

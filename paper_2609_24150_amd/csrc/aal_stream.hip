@@ -15,74 +15,15 @@
 // fast path for shapes it supports.
 #include "aal_device.h"
 #include "aal_internal.h"
+#include "aal_rowops.h"
 
 #include <limits.h>
 
 namespace aal {
 namespace {
 
-constexpr int kBlock = 256;
-constexpr int kWaves = kBlock / kWave;
-
-// Element group `gi` of a row: one 16-byte vector (VEC) or one element.
-template <class TI, bool VEC>
-struct Groups {
-  static constexpr int E = VEC ? TI::kVec : 1;
-  static __device__ __forceinline__ void load(const void* base, int64_t g0, int64_t gi, float (&x)[E]) {
-    if constexpr (VEC) {
-      TI::unpack(ldvec(base, g0 + gi), x);
-    } else {
-      x[0] = TI::load1(base, g0 + gi);
-    }
-  }
-};
-
-__device__ LseState block_lse(LseState st, float sc, LseState* sh) {
-  st = wave_lse(st, sc);
-  const int w = threadIdx.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) sh[w] = st;
-  __syncthreads();
-  LseState r = sh[0];
-#pragma unroll
-  for (int i = 1; i < kWaves; ++i) r = lse_merge(r, sh[i], sc);
-  __syncthreads();
-  return r;
-}
-
-__device__ float block_sum(float v, float* sh) {
-  v = wave_sum(v);
-  const int w = threadIdx.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) sh[w] = v;
-  __syncthreads();
-  float r = sh[0];
-#pragma unroll
-  for (int i = 1; i < kWaves; ++i) r += sh[i];
-  __syncthreads();
-  return r;
-}
-
-// Largest value, lowest index among equal values.
-__device__ int block_argmax(float best, int idx, float* shf, int* shi) {
-  const float wm = wave_max(best);
-  const int wi = wave_min_i(best == wm ? idx : INT_MAX);
-  const int w = threadIdx.x / kWave;
-  if ((threadIdx.x & (kWave - 1)) == 0) {
-    shf[w] = wm;
-    shi[w] = wi;
-  }
-  __syncthreads();
-  float m = shf[0];
-  int i = shi[0];
-#pragma unroll
-  for (int k = 1; k < kWaves; ++k) {
-    if (shf[k] > m || (shf[k] == m && shi[k] < i)) {
-      m = shf[k];
-      i = shi[k];
-    }
-  }
-  __syncthreads();
-  return i;
-}
+constexpr int kBlock = kRowBlock;
+constexpr int kWaves = kRowWaves;
 
 template <class TI, int MODE, bool VEC, int U>
 __global__ __launch_bounds__(kBlock) void k_row_stats(const void* __restrict__ zd, const void* __restrict__ zt,

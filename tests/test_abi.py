@@ -28,6 +28,7 @@ def lib():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("aal_eal_fwd_bwd", "aal_wtv_fwd_bwd", "aal_sim_accept_grpo", "aal_workspace_bytes",
+              "aal_loss_fwd_bwd", "aal_loss_workspace_bytes",
               "aal_status_string", "aal_last_error", "aal_version"):
         assert n in names
 
@@ -95,3 +96,35 @@ def test_wtv_and_sim_validation(lib):
     assert sim(eps=-1.0) == 1
     assert sim(wsb=8) == 4
     assert sim(ws=8) == 3
+
+
+def test_loss_workspace_bytes(lib):
+    L = lib.lib()
+    a = L.aal_loss_workspace_bytes(0, 2048, 0, 7)
+    b = L.aal_loss_workspace_bytes(1, 4, 2048, 7)
+    assert a > 0 and b > 0 and a % 256 == 0 and b % 256 == 0
+    assert L.aal_loss_workspace_bytes(1, 2, 0, 7) == 0
+    assert L.aal_loss_workspace_bytes(5, 2, 8, 7) == 0
+    assert L.aal_loss_workspace_bytes(0, 0, 0, 7) == 0
+
+
+def _loss(L, lib, **kw):
+    a = dict(zd=16, zt=16, lab=None, dt=0, lay=1, B=2, S=9, K=3, V=8, Td=1.0, Tt=1.0, w=(1.0, 0.0, 0.0, 0.0),
+             loss=16, grad=None, gdt=0, ws=256, wsb=1 << 30)
+    a.update(kw)
+    return L.aal_loss_fwd_bwd(a["zd"], a["zt"], a["lab"], a["dt"], a["lay"], a["B"], a["S"], a["K"], a["V"],
+                              a["Td"], a["Tt"], lib.LossWeights(*a["w"]), a["loss"], None, None, None, None, None,
+                              None, a["grad"], a["gdt"], None, a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(lay=3), 1), (dict(B=0), 1), (dict(K=0), 1), (dict(K=65), 1), (dict(V=0), 1), (dict(S=0), 1),
+    (dict(Td=0.0), 1), (dict(Tt=float("nan")), 1), (dict(w=(float("inf"), 0, 0, 0)), 1),
+    (dict(zd=None), 1), (dict(zt=None), 1), (dict(zt=None, w=(0, 1.0, 0, 0)), 1), (dict(loss=None), 1),
+    (dict(dt=5), 2), (dict(grad=16, gdt=7), 2), (dict(zd=20), 3), (dict(grad=40), 3),
+    (dict(ws=None), 4), (dict(ws=64), 3), (dict(wsb=1000), 4), (dict(B=1 << 30, S=4), 1),
+])
+def test_loss_validation(lib, kw, code):
+    L = lib.lib()
+    assert _loss(L, lib, **kw) == code
+    assert L.aal_last_error().decode() != ""

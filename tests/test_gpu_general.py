@@ -1,0 +1,141 @@
+"""GPU parity of the combined-objective entry point (aal_loss_fwd_bwd) with
+the fp64 oracle: disjoint windows and sliding windows over sequences, every
+term alone and in the paper's combinations, both dtypes, ragged and
+multi-tile vocabularies, labels, grad_scale, and windows that do not fit.
+
+Tolerances are those of tests/parity.py; the gradient coefficient of a row
+for the elementwise bound is |coef_tv| + |coef_eal| + |coef_kl| (each term's
+gradient is that coefficient times a vector bounded by 1 in magnitude)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from parity import check_grad, host64, rel_err, KAPPA
+
+pytestmark = pytest.mark.gpu
+
+WIN, SEQ = 0, 1
+
+
+@pytest.fixture(scope="module")
+def A():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_24150_amd as lib
+    return lib
+
+
+def _inputs(B, S, V, dtype, seed, peaks=True):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    zt = torch.randn(B, S, V, generator=g) * 2.5
+    if peaks:
+        idx = torch.randint(0, V, (B, S, 3), generator=g)
+        zt.scatter_add_(-1, idx, torch.full((B, S, 3), 6.0))
+    zd = 0.7 * zt + torch.randn(B, S, V, generator=g) * 1.5
+    return zd.to(dtype).cuda(), zt.to(dtype).cuda()
+
+
+def _check(A, zd, zt, K, weights, layout, Td=1.0, Tt=1.0, labels=None, gdt=None, scale=None, pass_target=True):
+    B, S, V = zd.shape
+    r = A.aal_loss_fwd_bwd(zd, zt if pass_target else None, K, weights=weights, temp_draft=Td, temp_target=Tt,
+                           layout=layout, labels=labels, grad_dtype=gdt,
+                           grad_scale=None if scale is None else torch.tensor([scale], device=zd.device))
+    torch.cuda.synchronize()
+    zd64, zt64 = host64(zd), host64(zt)
+    lab = None if labels is None else labels.cpu().numpy()
+    o = O.combined_loss(zd64, zt64, Td, Tt, weights, layout, B, S, K, labels=lab,
+                        grad_scale=1.0 if scale is None else scale)
+    f32 = zd.dtype == torch.float32
+    rtol, atol = (1e-5, 1e-6) if f32 else (1e-3, 1e-5)
+    terms = host64(r["terms"])
+    on = np.array([w != 0 for w in weights])
+    assert np.all(terms[~on] == 0.0)  # terms with weight 0 are not evaluated
+    assert np.all(np.abs(terms - o["terms"])[on] <= (rtol * np.abs(o["terms"]) + atol)[on]), (terms, o["terms"])
+    assert abs(r["loss"].item() - o["loss"]) <= rtol * abs(o["loss"]) + atol * 4
+    W = len(o["E_tv"])
+    if W and (weights[0] or weights[3]):
+        assert rel_err(host64(r["E_tv"]), o["E_tv"]) <= rtol
+    if W and weights[1]:
+        assert rel_err(host64(r["E_eal"]), o["E_eal"]) <= rtol
+    if weights[1]:
+        assert np.array_equal(r["xstar"].cpu().numpy(), o["xstar"])
+        np.testing.assert_allclose(host64(r["accept_eal"]), o["a_eal"], rtol=rtol, atol=1e-7)
+    if weights[0] or weights[2] or weights[3]:
+        np.testing.assert_allclose(host64(r["accept_tv"]), o["a_tv"], rtol=rtol, atol=1e-6 if f32 else 1e-4)
+    else:
+        assert not r["accept_tv"].any()
+    if not weights[1]:
+        assert not r["accept_eal"].any() and bool((r["xstar"] == -1).all())
+    coef = np.abs(o["coef_tv"]) + np.abs(o["coef_eal"]) + np.abs(o["coef_kl"])
+    q = np.exp(O.tempered_log_softmax(zd64.reshape(-1, V), Td))
+    p = np.exp(O.tempered_log_softmax(zt64.reshape(-1, V), Tt))
+    near = np.abs(q - p) <= 1e-5 * np.maximum(p, q)
+    qtie = np.max(np.where(near, q, 0.0), axis=-1)
+    rows = np.abs(o["coef_tv"]) * qtie * q.max(-1) > 0.25 * KAPPA * coef
+    elems = near if (weights[0] or weights[3]) else None
+    return check_grad(host64(r["grad"]), o["grad"], coef, zd.dtype, r["grad"].dtype,
+                      exclude_rows=rows if elems is not None else None, exclude_elems=elems)
+
+
+WEIGHTS = [(1, 0, 0, 0), (0, 1, 0, 0), (0, 0, 1, 0), (0, 0, 0, 1), (0, 0.1, 1, 0), (0, 0, 1, 1),
+           (0.7, 0.4, 1.3, 0.9)]
+
+
+@pytest.mark.parametrize("weights", WEIGHTS)
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_sequences_all_terms(A, weights, dtype):
+    zd, zt = _inputs(3, 11, 1000, dtype, seed=1)
+    _check(A, zd, zt, 4, weights, SEQ, Td=0.8, Tt=1.2)
+
+
+@pytest.mark.parametrize("weights", WEIGHTS)
+def test_windows_all_terms(A, weights):
+    zd, zt = _inputs(5, 4, 3000, torch.bfloat16, seed=2)
+    _check(A, zd, zt, 4, weights, WIN)
+
+
+@pytest.mark.parametrize("S,K", [(7, 7), (5, 7), (1, 1), (9, 1), (40, 16)])
+def test_sequence_edges(A, S, K):
+    zd, zt = _inputs(2, S, 257, torch.float32, seed=3 + S + K)
+    _check(A, zd, zt, K, (0.7, 0.4, 1.3, 0.9), SEQ, Td=0.7, Tt=0.7)
+
+
+@pytest.mark.parametrize("V", [1, 3, 130, 2047, 2051])
+def test_ragged_vocab(A, V):
+    zd, zt = _inputs(2, 6, V, torch.bfloat16, seed=10 + V, peaks=V > 8)
+    _check(A, zd, zt, 3, (0.7, 0.4, 1.3, 0.9), SEQ, Td=1.1, Tt=0.9)
+
+
+def test_fp32_grad_from_bf16_and_scale(A):
+    zd, zt = _inputs(2, 9, 777, torch.bfloat16, seed=20)
+    _check(A, zd, zt, 3, (0.7, 0.4, 1.3, 0.9), SEQ, gdt=torch.float32, scale=3.5)
+
+
+def test_labels_and_target_free_eal(A):
+    zd, zt = _inputs(2, 9, 512, torch.float32, seed=21)
+    g = torch.Generator(device="cpu").manual_seed(5)
+    lab = torch.randint(0, 512, (2 * 9,), generator=g, dtype=torch.int32).cuda()
+    _check(A, zd, zt, 3, (0, 1, 0, 0), SEQ, labels=lab)
+    _check(A, zd, zt, 3, (0, 1, 0, 0), SEQ, labels=lab, pass_target=False)
+    _check(A, zd, zt, 3, (0.5, 0.1, 1.0, 0.3), SEQ, labels=lab)
+
+
+def test_kl_of_identical_distributions_is_zero(A):
+    zd, _ = _inputs(2, 5, 300, torch.float32, seed=22)
+    r = A.aal_loss_fwd_bwd(zd, zd.clone(), 3, weights=(0, 0, 1, 1), layout=SEQ)
+    torch.cuda.synchronize()
+    assert abs(r["terms"][2].item()) < 1e-6 and abs(r["terms"][3].item()) < 1e-6
+    assert r["grad"].abs().max().item() < 1e-6
+
+
+def test_sequences_match_resident_wtv_for_single_window_sequences(A):
+    """S = K: every sequence is one window, so the combined entry point and the
+    fused WTV kernel compute the same loss and gradient."""
+    zd, zt = _inputs(64, 7, 4096, torch.bfloat16, seed=23)
+    r = A.aal_loss_fwd_bwd(zd, zt, 7, weights=(1, 0, 0, 0), layout=SEQ)
+    w = A.aal_wtv_fwd_bwd(zd, zt, 1.0, 1.0)
+    torch.cuda.synchronize()
+    assert rel_err(r["loss"].item(), w["loss"].item()) < 1e-5
+    d = (r["grad"].float() - w["grad"].float()).abs().max().item()
+    assert d <= 2 * w["grad"].float().abs().max().item() * 2 ** -8
