@@ -12,8 +12,10 @@ Prints ONE JSON line.  `value` is logit rows/s; `roofline` prices the step
 against HBM bandwidth with the algorithmic byte count (both logit tensors read
 once, the gradient written once: (2 s_in + s_grad) V bytes per row) over the
 average step time measured with HIP events on the stream the kernels run on.
-Secondary measurements (EAL on the same inputs, the simulated-acceptance
-reward on the GRPO workload) are reported under "also".  `cpu_baseline` times
+Secondary measurements (EAL on the same inputs; the combined-objective entry
+point on the same rows read as sliding-window sequences and with the paper's
+KL-anchored objectives; the simulated-acceptance reward on the GRPO workload)
+are reported under "also".  `cpu_baseline` times
 the fp64 oracle on a bounded sample of the same workload on the host cores.
 """
 from __future__ import annotations
@@ -185,6 +187,33 @@ def sim_call(inp):
     return fn, stream
 
 
+def general_call(zd, zt, layout, B, S, K, weights, grad_dtype):
+    """A zero-allocation closure over aal_loss_fwd_bwd (combined objectives)."""
+    import torch
+
+    from paper_2609_24150_amd import _lib
+    V = zd.shape[-1]
+    dev = zd.device
+    R = B * S
+    W = B if layout == _lib.AAL_LAYOUT_WINDOWS else B * max(0, S - K + 1)
+    L = _lib.lib()
+    loss = torch.empty(1, device=dev)
+    terms = torch.empty(4, device=dev)
+    grad = torch.empty(R, V, dtype=grad_dtype, device=dev)
+    ws = torch.empty(L.aal_loss_workspace_bytes(layout, B, S, K), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    dcode = _lib.AAL_BF16 if zd.dtype == torch.bfloat16 else _lib.AAL_F32
+    gcode = _lib.AAL_BF16 if grad_dtype == torch.bfloat16 else _lib.AAL_F32
+    w = _lib.LossWeights(*weights)
+
+    def fn():
+        st = L.aal_loss_fwd_bwd(zd.data_ptr(), zt.data_ptr(), None, dcode, layout, B, S, K, V, 1.0, 1.0, w,
+                                loss.data_ptr(), terms.data_ptr(), None, None, None, None, None, grad.data_ptr(),
+                                gcode, None, ws.data_ptr(), ws.numel(), stream.cuda_stream)
+        _lib.check(st, "aal_loss_fwd_bwd")
+    return fn, stream, R, W
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -260,6 +289,20 @@ def main():
         ms_e = _time_calls(fn_e, args.steps, args.warmup, st_e)
         also["eal_same_inputs"] = {"ms": ms_e, "rows_per_s": rows / (ms_e * 1e-3),
                                    "alg_GBps": rows * (2 * s_in + s_g) * V / (ms_e * 1e-3) / 1e9}
+        if args.workload == "c2":
+            from paper_2609_24150_amd import _lib
+            zd, zt = inp["z_draft"], inp["z_target"]
+            # the same rows read as 7 sequences of 2048 positions, windows sliding by one
+            legs = [("wtv_sliding_7x2048", _lib.AAL_LAYOUT_SEQUENCES, 7, 2048, (1.0, 0.0, 0.0, 0.0)),
+                    ("kl_plus_0.1eal_c2", _lib.AAL_LAYOUT_WINDOWS, N, K, (0.0, 0.1, 1.0, 0.0)),
+                    ("kl_plus_tv_c2", _lib.AAL_LAYOUT_WINDOWS, N, K, (0.0, 0.0, 1.0, 1.0))]
+            for name, layout, B_, S_, wts in legs:
+                fn_g, st_g, R_, W_ = general_call(zd, zt, layout, B_, S_, K, wts, gdt)
+                ms_g = _time_calls(fn_g, args.steps, args.warmup, st_g)
+                also[name] = {"ms": ms_g, "rows_per_s": R_ / (ms_g * 1e-3), "windows_per_s": W_ / (ms_g * 1e-3),
+                              "alg_GBps": R_ * (2 * s_in + s_g) * V / (ms_g * 1e-3) / 1e9,
+                              "entry": "aal_loss_fwd_bwd", "weights(wtv,eal,kl,tv)": wts}
+            del zd, zt
         del inp
         torch.cuda.empty_cache()
         sim = make_config("c5", seed=0, device=dev)
