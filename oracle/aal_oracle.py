@@ -56,6 +56,9 @@ __all__ = [
     "forward_kl",
     "window_length_coefficients",
     "combined_loss",
+    "greedy_accepted_length",
+    "grpo_windows",
+    "grpo_loss",
 ]
 
 
@@ -405,6 +408,117 @@ def combined_loss(z_draft, z_target, T_draft: float, T_target: float, weights, l
     return {"loss": loss, "terms": terms, "E_tv": E_tv, "E_eal": E_eal, "a_tv": a_tv,
             "qlt": qlt, "a_eal": a_eal, "xstar": xs, "kl": kl, "grad": grad,
             "coef_tv": g_tv * f, "coef_eal": g_eal * a_eal * f, "coef_kl": g_kl * f}
+
+
+# ---------------------------------------------------------------------------
+# GRPO on the simulated greedy acceptance length (Section "GRPO Loss on
+# Acceptance Length": greedy trajectories, Eq. debiased_reward, the policy
+# ratio, Eq. advantage and the clipped surrogate)
+# ---------------------------------------------------------------------------
+def greedy_accepted_length(S_tokens, x_star) -> np.ndarray:
+    """tau = sum_{k=1..K} prod_{j<=k} 1[S_j = x*_j]: the number of leading
+    positions where the greedy draft token equals the target's token."""
+    match = (np.asarray(S_tokens) == np.asarray(x_star)).astype(np.int64)
+    return np.sum(np.cumprod(match, axis=-1), axis=-1)
+
+
+def grpo_windows(layout: int, n_groups_or_B: int, S: int, m: int, K: int, anchors=None) -> np.ndarray:
+    """Row indices [n_groups, m, K] of the windows of every group.
+
+    Windows layout: rows are [n_groups * m * K]; group g holds windows
+    g*m .. g*m+m-1, each K consecutive rows.  Sequences layout: B sequences of
+    S positions and ``anchors`` [B, G] (start of each group's first window);
+    group (b, g) holds the m windows starting at anchor, anchor+1, ...,
+    anchor+m-1, each covering K consecutive positions (all sliced from the one
+    forward pass over the sequence)."""
+    if layout == LAYOUT_WINDOWS:
+        return np.arange(n_groups_or_B * m * K, dtype=np.int64).reshape(n_groups_or_B, m, K)
+    B = n_groups_or_B
+    a = np.asarray(anchors, np.int64).reshape(B, -1)
+    G = a.shape[1]
+    starts = (np.arange(B)[:, None] * S + a)[:, :, None] + np.arange(m)[None, None, :]  # [B, G, m]
+    rows = starts[..., None] + np.arange(K)  # [B, G, m, K]
+    return rows.reshape(B * G, m, K)
+
+
+def grpo_loss(z_theta, z_ref, z_target, T: float, layout: int, B: int, S: int, m: int, K: int,
+              anchors=None, labels=None, eps: float = 1e-6, adv_clip: float = 0.0,
+              eps_clip: float = 0.2, rho_min: float = 0.0, rho_max: float = np.inf,
+              grad_scale: float = 1.0):
+    """GRPO loss on the debiased greedy acceptance length and its gradient
+    w.r.t. the current draft's logits ``z_theta`` (rows [R, V]).
+
+    Per window (K positions) of group g:
+      S^pi_k = argmax z_pi,k (lowest index on ties), for pi = theta and ref;
+      tau^pi = greedy_accepted_length(S^pi, x*), x* = labels or argmax z_target;
+      R = tau^theta - tau^ref (no gradient);
+      log rho = (1/K) sum_k [log pi_theta(S^theta_k) - log pi_ref(S^theta_k)],
+        pi = softmax(z / T), clipped to [-10, 10];
+      rho = clip(exp(log rho), rho_min, rho_max);
+      A = clip((R - mean_g R) / (std_g R + eps), -adv_clip, adv_clip)
+        (population std over the group's m windows; adv_clip <= 0: no clip;
+        no gradient);
+      L_g = -(1/m) sum_{windows of g} min(rho A, clip(rho, 1-eps_clip, 1+eps_clip) A);
+    loss = mean over all groups of L_g.
+
+    The gradient flows through log pi_theta only.  Conventions at kinks: the
+    derivative of a clip is taken as 1 strictly inside its interval and 0
+    elsewhere, and min(u, v) takes the derivative of u when u <= v.
+    d log pi_theta(S_k) / d z_theta,k(v) = (1/T) (1[v = S_k] - pi_theta,k(v)).
+
+    Returns a dict: loss, group_loss [n_groups], S_theta, S_ref, x_star [R],
+    tau_theta, tau_ref, reward, log_rho, rho, adv, coef [n_groups, m] (dloss /
+    dlog rho of each window), grad [R, V].
+    """
+    zth = np.asarray(z_theta, np.float64)
+    V = zth.shape[-1]
+    zth = zth.reshape(-1, V)
+    zrf = np.asarray(z_ref, np.float64).reshape(-1, V)
+    n_groups = B if layout == LAYOUT_WINDOWS else B * np.asarray(anchors).reshape(B, -1).shape[1]
+    win = grpo_windows(layout, B, S, m, K, anchors)  # [n_groups, m, K]
+
+    lth = tempered_log_softmax(zth, T)
+    lrf = tempered_log_softmax(zrf, T)
+    S_th = np.argmax(zth, axis=-1)
+    S_rf = np.argmax(zrf, axis=-1)
+    if labels is not None:
+        xs = np.asarray(labels, np.int64).reshape(-1)
+    else:
+        xs = greedy_token(np.asarray(z_target, np.float64).reshape(-1, V))
+    rows = np.arange(zth.shape[0])
+    lp_th = lth[rows, S_th]          # log pi_theta(S^theta)
+    lp_rf = lrf[rows, S_th]          # log pi_ref(S^theta)
+
+    tau_th = greedy_accepted_length(S_th[win], xs[win])   # [n_groups, m]
+    tau_rf = greedy_accepted_length(S_rf[win], xs[win])
+    reward = (tau_th - tau_rf).astype(np.float64)
+    lr_raw = np.mean(lp_th[win] - lp_rf[win], axis=-1)    # [n_groups, m]
+    log_rho = np.clip(lr_raw, -10.0, 10.0)
+    rho_e = np.exp(log_rho)
+    rho = np.clip(rho_e, rho_min, rho_max)
+    adv = group_advantage(reward, eps, 0, adv_clip if adv_clip > 0 else None)
+    clipped = np.clip(rho, 1.0 - eps_clip, 1.0 + eps_clip)
+    u = rho * adv
+    v = clipped * adv
+    surrogate = np.minimum(u, v)
+    group_loss = -np.mean(surrogate, axis=-1)
+    loss = np.mean(group_loss)
+
+    # dloss / d log rho, window by window
+    d_clip = ((rho > 1.0 - eps_clip) & (rho < 1.0 + eps_clip)).astype(np.float64)
+    d_sur_d_rho = np.where(u <= v, adv, adv * d_clip)
+    d_rho_d_lr = np.where((rho_e > rho_min) & (rho_e < rho_max) & (lr_raw > -10.0) & (lr_raw < 10.0), rho_e, 0.0)
+    coef = -(1.0 / (n_groups * m)) * d_sur_d_rho * d_rho_d_lr   # dloss/dlog rho
+    # log rho = (1/K) sum_k log pi_theta(S_k) - const: spread over the window's rows
+    row_coef = np.zeros(zth.shape[0])
+    np.add.at(row_coef, win.reshape(-1), np.repeat(coef.reshape(-1), K) / K)
+    pth = np.exp(lth)
+    onehot = np.zeros_like(pth)
+    onehot[rows, S_th] = 1.0
+    grad = (grad_scale * row_coef / T)[:, None] * (onehot - pth)
+    return {"loss": loss, "group_loss": group_loss, "S_theta": S_th, "S_ref": S_rf, "x_star": xs,
+            "tau_theta": tau_th, "tau_ref": tau_rf, "reward": reward, "log_rho": log_rho, "rho": rho,
+            "adv": adv, "coef": coef, "grad": grad}
 
 
 # ---------------------------------------------------------------------------
