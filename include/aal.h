@@ -10,7 +10,11 @@
  *     acceptance sum_v min(p~, q~) = 1 - TV (Eq. acc_sample, Eq. rejection_rate);
  *   - the simulated accepted-length reward and the group-relative advantage
  *     (Section "GRPO Loss on Acceptance Length", Eq. advantage), with the draft
- *     token drawn and verified by sampling verification (Eq. acc_sample).
+ *     token drawn and verified by sampling verification (Eq. acc_sample);
+ *   - sliding windows over sequences and the weighted objectives of the
+ *     experiments (forward-KL anchor, window-mean TV, EAL, WTV) in one call;
+ *   - the GRPO loss on the debiased greedy acceptance length with its
+ *     policy-ratio surrogate and gradient.
  * Temperature scaling is Eq. (1), i.e. softmax(z / T).  Window aggregation is
  * Eq. eal_generic: E[L] = sum_{k=1..K} prod_{j<k} a_j.
  *
@@ -226,6 +230,65 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
                               aal_loss_weights_t weights, float* loss, float* terms,
                               float* e_tv, float* e_eal, float* accept_tv, float* accept_eal,
                               int32_t* xstar, void* grad_draft, aal_dtype_t grad_dtype,
+                              const float* grad_scale, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+/* Constants of the GRPO loss that the paper leaves unstated (its Eq. advantage
+ * uses eps = 1e-6). */
+typedef struct {
+  float eps;      /* advantage denominator: (R - mean) / (std + eps), eps >= 0        */
+  float adv_clip; /* C_A: advantages clipped to [-C_A, C_A]; <= 0 disables the clip   */
+  float eps_clip; /* PPO clip of the ratio: [1 - eps_clip, 1 + eps_clip], >= 0        */
+  float rho_min;  /* ratio clip before the surrogate: [rho_min, rho_max],             */
+  float rho_max;  /*   0 <= rho_min <= rho_max (rho_max may be +inf)                   */
+} aal_grpo_params_t;
+
+/* Workspace bytes of aal_grpo_fwd_bwd (0 for invalid arguments). */
+size_t aal_grpo_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32_t G, int32_t m, int32_t K);
+
+/*
+ * GRPO loss on the debiased greedy acceptance length, forward and backward
+ * w.r.t. the current draft's logits (Section "GRPO Loss on Acceptance
+ * Length": greedy trajectories S^theta, S^ref; simulated greedy
+ * verification; Eq. debiased_reward; the per-token geometric-mean policy
+ * ratio clipped to [-10, 10]; Eq. advantage; the PPO-clipped group loss and
+ * its mean over groups).
+ *
+ * Per window of K positions (rows r_0..r_{K-1}) of a group of m windows:
+ *   S^pi_k   = argmax_v z_pi[r_k, v]  (pi = theta, ref; lowest index on ties)
+ *   tau^pi   = number of leading k with S^pi_k = x*_k, x* = labels or argmax z_target
+ *   R        = tau^theta - tau^ref                       (no gradient)
+ *   log rho  = clip((1/K) sum_k [log pi_theta(S^theta_k) - log pi_ref(S^theta_k)], -10, 10),
+ *              pi = softmax(z / temperature)
+ *   rho      = clip(exp(log rho), rho_min, rho_max)
+ *   A        = clip((R - mean_g R) / (std_g R + eps), -adv_clip, adv_clip)  (population
+ *              std over the group's m windows; no gradient)
+ *   L_g      = -(1/m) sum_windows min(rho A, clip(rho, 1 - eps_clip, 1 + eps_clip) A)
+ *   loss     = mean over groups of L_g
+ *   grad_theta[r, v] = scale * sum over windows w containing r of
+ *              (dloss/dlog rho_w) (1/K) (1/temperature) (1[v = S^theta_r] - pi_theta,r(v)),
+ *   where a clip passes derivative 1 strictly inside its interval and 0 elsewhere,
+ *   and min(u, v) takes u's derivative when u <= v.
+ *
+ * Layouts: AAL_LAYOUT_WINDOWS: logits [B*m*K, V]: B groups of m windows of K
+ *   rows each (S, G, anchors ignored).  AAL_LAYOUT_SEQUENCES: logits [B*S, V]:
+ *   B sequences of S positions and anchors [B*G] int32; group (b, g) holds
+ *   the m windows starting at anchors[b*G+g] + i, i < m (anchors are clamped
+ *   into [0, S - m - K + 1]).  Rows in no window get a zero gradient.
+ * z_theta, z_ref : [rows, V] of in_dtype, required.  z_target : [rows, V] or
+ *   NULL when labels [rows] int32 are given (clamped into [0, V)).
+ * B >= 1, 1 <= K <= 64, 1 <= m <= 64, V >= 1; sequences: G >= 1 and S >= m + K - 1;
+ * temperature finite and > 0; params as documented at aal_grpo_params_t.
+ * loss : [1] float, required.  tau_theta, tau_ref : [groups*m] int32, or NULL.
+ * advantage, log_rho : [groups*m] float (the clipped log rho), or NULL.
+ * grad_theta, grad_dtype, grad_scale : as for aal_eal_fwd_bwd.
+ */
+aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void* z_target,
+                              const int32_t* labels, aal_dtype_t in_dtype, aal_layout_t layout,
+                              int64_t B, int32_t S, int32_t G, int32_t m, int32_t K, int32_t V,
+                              const int32_t* anchors, float temperature, aal_grpo_params_t params,
+                              float* loss, int32_t* tau_theta, int32_t* tau_ref, float* advantage,
+                              float* log_rho, void* grad_theta, aal_dtype_t grad_dtype,
                               const float* grad_scale, void* workspace, size_t workspace_bytes,
                               void* stream);
 

@@ -11,6 +11,8 @@ from .api import (  # noqa: F401
     AAL_LAYOUT_SEQUENCES,
     AAL_LAYOUT_WINDOWS,
     aal_eal_fwd_bwd,
+    aal_grpo_fwd_bwd,
+    aal_grpo_workspace_bytes,
     aal_loss_fwd_bwd,
     aal_loss_workspace_bytes,
     aal_sim_accept_grpo,

@@ -28,6 +28,12 @@ class LossWeights(C.Structure):
     _fields_ = [("wtv", C.c_float), ("eal", C.c_float), ("kl", C.c_float), ("tv", C.c_float)]
 
 
+class GrpoParams(C.Structure):
+    """aal_grpo_params_t (passed by value)."""
+    _fields_ = [("eps", C.c_float), ("adv_clip", C.c_float), ("eps_clip", C.c_float),
+                ("rho_min", C.c_float), ("rho_max", C.c_float)]
+
+
 _vp = C.c_void_p
 _SIGNATURES = {
     "aal_version": (C.c_int, []),
@@ -53,6 +59,11 @@ _SIGNATURES = {
     "aal_loss_fwd_bwd": (C.c_int, [
         _vp, _vp, _vp, C.c_int, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_float, C.c_float,
         LossWeights, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+        _vp, C.c_int, _vp, _vp, C.c_size_t, _vp]),
+    "aal_grpo_workspace_bytes": (C.c_size_t, [C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
+    "aal_grpo_fwd_bwd": (C.c_int, [
+        _vp, _vp, _vp, _vp, C.c_int, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+        C.c_int32, _vp, C.c_float, GrpoParams, _vp, _vp, _vp, _vp, _vp,
         _vp, C.c_int, _vp, _vp, C.c_size_t, _vp]),
 }
 

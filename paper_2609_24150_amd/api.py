@@ -203,3 +203,61 @@ def aal_loss_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor | None, K: in
         _ptr(ws), ws.numel(), _stream(dev, stream))
     _lib.check(st, "aal_loss_fwd_bwd")
     return out
+
+
+def aal_grpo_workspace_bytes(layout: int, B: int, S: int, G: int, m: int, K: int) -> int:
+    return int(_lib.lib().aal_grpo_workspace_bytes(int(layout), int(B), int(S), int(G), int(m), int(K)))
+
+
+def aal_grpo_fwd_bwd(z_theta: torch.Tensor, z_ref: torch.Tensor, z_target: torch.Tensor | None, m: int, K: int, *,
+                     layout: int = AAL_LAYOUT_WINDOWS, anchors: torch.Tensor | None = None,
+                     labels: torch.Tensor | None = None, temperature: float = 1.0, eps: float = 1e-6,
+                     adv_clip: float = 0.0, eps_clip: float = 0.2, rho_min: float = 0.0,
+                     rho_max: float = float("inf"), grad: bool = True, grad_dtype: torch.dtype | None = None,
+                     grad_scale: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> dict:
+    """GRPO loss on the debiased greedy acceptance length, forward + backward
+    w.r.t. z_theta.
+
+    Windows layout: logits [B, m*K, V] (B groups of m windows of K rows).
+    Sequences layout: logits [B, S, V] and anchors int32 [B, G].
+    Returns a dict: loss [1], tau_theta, tau_ref [groups, m] int32,
+    advantage, log_rho [groups, m], grad (the logits' shape, or None)."""
+    for t in (z_theta, z_ref) + ((z_target,) if z_target is not None else ()):
+        if t.dim() != 3 or not t.is_cuda or not t.is_contiguous() or t.shape != z_theta.shape or t.dtype != z_theta.dtype:
+            raise ValueError("logits must be contiguous device tensors of one shape [B, rows, V] and dtype")
+    B, S, V = z_theta.shape
+    dev = z_theta.device
+    if layout == AAL_LAYOUT_WINDOWS:
+        if S != m * K:
+            raise ValueError("windows layout needs logits of shape [groups, m*K, V]")
+        G, groups = 1, B
+    else:
+        if anchors is None or anchors.dim() != 2 or anchors.shape[0] != B or anchors.dtype != torch.int32:
+            raise ValueError("sequences layout needs int32 anchors of shape [B, G]")
+        G = anchors.shape[1]
+        groups = B * G
+        anchors = anchors.contiguous()
+    if labels is not None and (labels.dtype != torch.int32 or labels.numel() != B * S or labels.device != dev):
+        raise ValueError("labels must be an int32 device tensor with one entry per row")
+    if grad_scale is not None and (grad_scale.dtype != torch.float32 or grad_scale.device != dev):
+        raise TypeError("grad_scale must be a float32 device tensor")
+    out = {
+        "loss": torch.empty(1, dtype=torch.float32, device=dev),
+        "tau_theta": torch.empty(groups, m, dtype=torch.int32, device=dev),
+        "tau_ref": torch.empty(groups, m, dtype=torch.int32, device=dev),
+        "advantage": torch.empty(groups, m, dtype=torch.float32, device=dev),
+        "log_rho": torch.empty(groups, m, dtype=torch.float32, device=dev),
+        "grad": torch.empty(B, S, V, dtype=grad_dtype or z_theta.dtype, device=dev) if grad else None,
+    }
+    if ws is None:
+        ws = torch.empty(aal_grpo_workspace_bytes(layout, B, S, G, m, K), dtype=torch.uint8, device=dev)
+    g = out["grad"]
+    prm = _lib.GrpoParams(float(eps), float(adv_clip), float(eps_clip), float(rho_min), float(rho_max))
+    st = _lib.lib().aal_grpo_fwd_bwd(
+        _ptr(z_theta), _ptr(z_ref), _ptr(z_target), _ptr(labels), _dtype_code(z_theta.dtype), int(layout),
+        B, S, G, m, K, V, _ptr(anchors), float(temperature), prm, _ptr(out["loss"]), _ptr(out["tau_theta"]),
+        _ptr(out["tau_ref"]), _ptr(out["advantage"]), _ptr(out["log_rho"]),
+        _ptr(g), _dtype_code(g.dtype) if g is not None else AAL_F32, _ptr(grad_scale),
+        _ptr(ws), ws.numel(), _stream(dev, stream))
+    _lib.check(st, "aal_grpo_fwd_bwd")
+    return out

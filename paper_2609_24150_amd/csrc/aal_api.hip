@@ -340,4 +340,114 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
   return AAL_OK;
 }
 
+size_t aal_grpo_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32_t G, int32_t m, int32_t K) {
+  if (B < 1 || K < 1 || m < 1) return 0;
+  if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES) return 0;
+  if (layout == AAL_LAYOUT_SEQUENCES && (G < 1 || S < 1)) return 0;
+  const int64_t groups = layout == AAL_LAYOUT_WINDOWS ? B : B * G;
+  const int64_t rows = layout == AAL_LAYOUT_WINDOWS ? B * m * K : B * S;
+  return aal::grpo_workspace_bytes(rows, groups, groups * m);
+}
+
+aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void* z_target, const int32_t* labels,
+                              aal_dtype_t in_dtype, aal_layout_t layout, int64_t B, int32_t S, int32_t G, int32_t m,
+                              int32_t K, int32_t V, const int32_t* anchors, float temperature,
+                              aal_grpo_params_t params, float* loss, int32_t* tau_theta, int32_t* tau_ref,
+                              float* advantage, float* log_rho, void* grad_theta, aal_dtype_t grad_dtype,
+                              const float* grad_scale, void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES)
+    return fail(AAL_ERR_ARG, "unknown layout %d", int(layout));
+  if (B < 1) return fail(AAL_ERR_ARG, "B must be >= 1 (got %lld)", (long long)B);
+  if (K < 1 || K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", K);
+  if (m < 1 || m > 64) return fail(AAL_ERR_ARG, "m must be in [1, 64] (got %d)", m);
+  if (V < 1) return fail(AAL_ERR_ARG, "V must be >= 1 (got %d)", V);
+  const bool seq = layout == AAL_LAYOUT_SEQUENCES;
+  if (seq) {
+    if (G < 1) return fail(AAL_ERR_ARG, "G must be >= 1 (got %d)", G);
+    if (S < m + K - 1) return fail(AAL_ERR_ARG, "S must be >= m + K - 1 (got S=%d, m=%d, K=%d)", S, m, K);
+    if (!anchors) return fail(AAL_ERR_ARG, "anchors must be non-NULL for the sequences layout");
+  }
+  const int64_t per = seq ? int64_t(S) : int64_t(m) * K;
+  if (B > ((int64_t(1) << 31) - 1) / per) return fail(AAL_ERR_ARG, "the number of rows must be < 2^31");
+  const int64_t R = B * per;
+  if (R > (int64_t(1) << 62) / V) return fail(AAL_ERR_ARG, "rows*V must be < 2^62");
+  const int64_t groups = seq ? B * G : B;
+  if (groups > (int64_t(1) << 31) / m) return fail(AAL_ERR_ARG, "groups*m must be < 2^31");
+  if (!z_theta || !z_ref) return fail(AAL_ERR_ARG, "z_theta and z_ref must be non-NULL");
+  if (!z_target && !labels) return fail(AAL_ERR_ARG, "z_target or labels must be given");
+  if (!loss) return fail(AAL_ERR_ARG, "loss must be non-NULL");
+  if (!valid_dtype(int(in_dtype))) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", int(in_dtype));
+  if (grad_theta && !valid_dtype(int(grad_dtype))) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", int(grad_dtype));
+  if (!aligned(z_theta, 16) || !aligned(z_ref, 16) || (z_target && !aligned(z_target, 16)))
+    return fail(AAL_ERR_ALIGN, "logit pointers must be 16-byte aligned");
+  if (grad_theta && !aligned(grad_theta, 16)) return fail(AAL_ERR_ALIGN, "grad_theta must be 16-byte aligned");
+  const float sc = scale_for(temperature);
+  if (!positive_finite(temperature) || sc == 0.f)
+    return fail(AAL_ERR_ARG, "temperature must be finite, > 0 and >= 1e-37");
+  auto finite_nonneg = [](float x) {
+    uint32_t u;
+    memcpy(&u, &x, sizeof u);
+    return (u >> 31) == 0 && ((u >> 23) & 0xffu) != 0xffu;
+  };
+  auto nonneg = [](float x) {
+    uint32_t u;
+    memcpy(&u, &x, sizeof u);
+    return (u >> 31) == 0 && !(((u >> 23) & 0xffu) == 0xffu && (u & 0x7fffffu) != 0);  // +inf allowed, NaN not
+  };
+  uint32_t ac;
+  memcpy(&ac, &params.adv_clip, sizeof ac);
+  if (!finite_nonneg(params.eps)) return fail(AAL_ERR_ARG, "eps must be finite and >= 0");
+  if (((ac >> 23) & 0xffu) == 0xffu) return fail(AAL_ERR_ARG, "adv_clip must be finite");
+  if (!finite_nonneg(params.eps_clip)) return fail(AAL_ERR_ARG, "eps_clip must be finite and >= 0");
+  if (!finite_nonneg(params.rho_min) || !nonneg(params.rho_max) || params.rho_max < params.rho_min)
+    return fail(AAL_ERR_ARG, "need 0 <= rho_min <= rho_max (rho_min finite)");
+  if (!workspace) return fail(AAL_ERR_WORKSPACE, "workspace must be non-NULL");
+  if (!aligned(workspace, 256)) return fail(AAL_ERR_ALIGN, "workspace must be 256-byte aligned");
+  const size_t need = aal::grpo_workspace_bytes(R, groups, groups * m);
+  if (workspace_bytes < need)
+    return fail(AAL_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+  uint8_t* wp = static_cast<uint8_t*>(workspace);
+  aal::GrpoArgs a{};
+  a.in = to_dtype(in_dtype);
+  a.gd = to_dtype(grad_dtype);
+  a.zth = z_theta;
+  a.zrf = z_ref;
+  a.zt = labels ? nullptr : z_target;
+  a.labels = labels;
+  a.layout = int(layout);
+  a.B = B;
+  a.S = seq ? S : m * K;
+  a.G = seq ? G : 1;
+  a.m = m;
+  a.K = K;
+  a.V = V;
+  a.R = R;
+  a.n_groups = groups;
+  a.anchors = seq ? anchors : nullptr;
+  a.sc = sc;
+  a.inv_t = 1.0f / temperature;
+  a.eps = params.eps;
+  a.adv_clip = params.adv_clip;
+  a.eps_clip = params.eps_clip;
+  a.rho_min = params.rho_min;
+  a.rho_max = params.rho_max;
+  a.loss = loss;
+  a.tau_theta = tau_theta;
+  a.tau_ref = tau_ref;
+  a.advantage = advantage;
+  a.log_rho = log_rho;
+  a.grad = grad_theta;
+  a.grad_scale = grad_scale;
+  a.rows = reinterpret_cast<aal::GrpoRow*>(wp);
+  wp += aal::align256(size_t(R) * sizeof(aal::GrpoRow));
+  a.win_coef = reinterpret_cast<float*>(wp);
+  wp += aal::align256(size_t(groups * m) * sizeof(float));
+  a.group_loss = reinterpret_cast<float*>(wp);
+  a.stream = static_cast<hipStream_t>(stream);
+  hipError_t e = aal::launch_grpo(a);
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
 }  // extern "C"

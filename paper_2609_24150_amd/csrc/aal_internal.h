@@ -139,6 +139,53 @@ struct GenArgs {
 // Row pass, window scan, loss, gradient pass.  Handles every shape.
 hipError_t launch_general(const GenArgs& a);
 
+// Per-row quantities of the GRPO schedule.  32 bytes.
+struct GrpoRow {
+  int32_t s_theta;  // greedy token of the current draft
+  int32_t s_ref;    // greedy token of the reference draft
+  int32_t xstar;    // the target's greedy token or the label
+  float lp_theta;   // log pi_theta(s_theta), natural log
+  float lp_ref;     // log pi_ref(s_theta)
+  float msc, l2s;   // current draft: fl(max * sc), log2 of the sum
+  float pad;
+};
+static_assert(sizeof(GrpoRow) == 32, "GrpoRow layout");
+
+inline size_t grpo_workspace_bytes(int64_t rows, int64_t groups, int64_t windows) {
+  return align256(size_t(rows) * sizeof(GrpoRow)) + align256(size_t(windows) * sizeof(float)) +
+         align256(size_t(groups) * sizeof(float));
+}
+
+struct GrpoArgs {
+  DType in;
+  DType gd;
+  const void* zth;
+  const void* zrf;
+  const void* zt;          // null when labels are given
+  const int32_t* labels;   // may be null
+  int layout;
+  int64_t B;
+  int S, G, m, K, V;
+  int64_t R;               // rows
+  int64_t n_groups;
+  const int32_t* anchors;  // sequences layout
+  float sc, inv_t;
+  float eps, adv_clip, eps_clip, rho_min, rho_max;
+  float* loss;
+  int32_t* tau_theta;      // optional [n_groups * m]
+  int32_t* tau_ref;
+  float* advantage;
+  float* log_rho;
+  void* grad;              // may be null
+  const float* grad_scale; // may be null
+  GrpoRow* rows;           // workspace
+  float* win_coef;         // workspace [n_groups * m]
+  float* group_loss;       // workspace [n_groups]
+  hipStream_t stream;
+};
+
+hipError_t launch_grpo(const GrpoArgs& a);
+
 struct SimArgs {
   DType in;
   const void* zd;

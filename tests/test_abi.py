@@ -28,7 +28,7 @@ def lib():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("aal_eal_fwd_bwd", "aal_wtv_fwd_bwd", "aal_sim_accept_grpo", "aal_workspace_bytes",
-              "aal_loss_fwd_bwd", "aal_loss_workspace_bytes",
+              "aal_loss_fwd_bwd", "aal_loss_workspace_bytes", "aal_grpo_fwd_bwd", "aal_grpo_workspace_bytes",
               "aal_status_string", "aal_last_error", "aal_version"):
         assert n in names
 
@@ -127,4 +127,36 @@ def _loss(L, lib, **kw):
 def test_loss_validation(lib, kw, code):
     L = lib.lib()
     assert _loss(L, lib, **kw) == code
+    assert L.aal_last_error().decode() != ""
+
+
+def test_grpo_workspace_bytes(lib):
+    L = lib.lib()
+    assert L.aal_grpo_workspace_bytes(0, 64, 0, 0, 8, 7) > 0
+    assert L.aal_grpo_workspace_bytes(1, 4, 2048, 4, 8, 7) > 0
+    assert L.aal_grpo_workspace_bytes(1, 4, 2048, 0, 8, 7) == 0
+    assert L.aal_grpo_workspace_bytes(0, 0, 0, 0, 8, 7) == 0
+
+
+def _grpo(L, lib, **kw):
+    a = dict(zth=16, zrf=16, zt=16, lab=None, dt=0, lay=1, B=2, S=20, G=2, m=4, K=3, V=8, anc=16, T=1.0,
+             prm=(1e-6, 0.0, 0.2, 0.0, float("inf")), loss=16, grad=None, gdt=0, ws=256, wsb=1 << 30)
+    a.update(kw)
+    return L.aal_grpo_fwd_bwd(a["zth"], a["zrf"], a["zt"], a["lab"], a["dt"], a["lay"], a["B"], a["S"], a["G"],
+                              a["m"], a["K"], a["V"], a["anc"], a["T"], lib.GrpoParams(*a["prm"]), a["loss"],
+                              None, None, None, None, a["grad"], a["gdt"], None, a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(lay=4), 1), (dict(B=0), 1), (dict(K=0), 1), (dict(K=65), 1), (dict(m=0), 1), (dict(m=65), 1),
+    (dict(V=0), 1), (dict(G=0), 1), (dict(S=5), 1), (dict(anc=None), 1), (dict(zth=None), 1),
+    (dict(zt=None), 1), (dict(loss=None), 1), (dict(T=0.0), 1),
+    (dict(prm=(-1.0, 0.0, 0.2, 0.0, 1.0)), 1), (dict(prm=(0.0, float("nan"), 0.2, 0.0, 1.0)), 1),
+    (dict(prm=(0.0, 0.0, -0.1, 0.0, 1.0)), 1), (dict(prm=(0.0, 0.0, 0.2, 2.0, 1.0)), 1),
+    (dict(prm=(0.0, 0.0, 0.2, 0.0, float("nan"))), 1), (dict(dt=3), 2), (dict(grad=16, gdt=3), 2),
+    (dict(zrf=24), 3), (dict(grad=8), 3), (dict(ws=None), 4), (dict(ws=32), 3), (dict(wsb=64), 4),
+])
+def test_grpo_validation(lib, kw, code):
+    L = lib.lib()
+    assert _grpo(L, lib, **kw) == code
     assert L.aal_last_error().decode() != ""
