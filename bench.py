@@ -214,6 +214,36 @@ def general_call(zd, zt, layout, B, S, K, weights, grad_dtype):
     return fn, stream, R, W
 
 
+def grpo_call(zth, zref, zt, m, K, grad_dtype):
+    """A zero-allocation closure over aal_grpo_fwd_bwd (windows layout, groups of m windows)."""
+    import torch
+
+    from paper_2609_24150_amd import _lib
+    B, S, V = zth.shape
+    dev = zth.device
+    L = _lib.lib()
+    loss = torch.empty(1, device=dev)
+    tt = torch.empty(B, m, dtype=torch.int32, device=dev)
+    tr = torch.empty_like(tt)
+    adv = torch.empty(B, m, device=dev)
+    lrho = torch.empty_like(adv)
+    grad = torch.empty(B, S, V, dtype=grad_dtype, device=dev)
+    ws = torch.empty(L.aal_grpo_workspace_bytes(_lib.AAL_LAYOUT_WINDOWS, B, S, 1, m, K), dtype=torch.uint8,
+                     device=dev)
+    stream = torch.cuda.current_stream(dev)
+    dcode = _lib.AAL_BF16 if zth.dtype == torch.bfloat16 else _lib.AAL_F32
+    gcode = _lib.AAL_BF16 if grad_dtype == torch.bfloat16 else _lib.AAL_F32
+    prm = _lib.GrpoParams(1e-6, 0.0, 0.2, 0.0, float("inf"))
+
+    def fn():
+        st = L.aal_grpo_fwd_bwd(zth.data_ptr(), zref.data_ptr(), zt.data_ptr(), None, dcode,
+                                _lib.AAL_LAYOUT_WINDOWS, B, S, 1, m, K, V, None, 1.0, prm, loss.data_ptr(),
+                                tt.data_ptr(), tr.data_ptr(), adv.data_ptr(), lrho.data_ptr(), grad.data_ptr(),
+                                gcode, None, ws.data_ptr(), ws.numel(), stream.cuda_stream)
+        _lib.check(st, "aal_grpo_fwd_bwd")
+    return fn, stream
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -302,7 +332,18 @@ def main():
                 also[name] = {"ms": ms_g, "rows_per_s": R_ / (ms_g * 1e-3), "windows_per_s": W_ / (ms_g * 1e-3),
                               "alg_GBps": R_ * (2 * s_in + s_g) * V / (ms_g * 1e-3) / 1e9,
                               "entry": "aal_loss_fwd_bwd", "weights(wtv,eal,kl,tv)": wts}
-            del zd, zt
+            # GRPO over the same rows: 256 groups of m=8 windows; the reference
+            # policy's logits are the draft's plus seeded noise
+            m_ = 8
+            g_ = torch.Generator(device=dev).manual_seed(11)
+            zref = (zd.float() + 0.5 * torch.randn(zd.shape, generator=g_, device=dev)).to(zd.dtype)
+            shp = (N // m_, m_ * K, V)
+            fn_r, st_r = grpo_call(zd.view(shp), zref.view(shp), zt.view(shp), m_, K, gdt)
+            ms_r = _time_calls(fn_r, args.steps, args.warmup, st_r)
+            also["grpo_c2_m8"] = {"ms": ms_r, "rows_per_s": rows / (ms_r * 1e-3),
+                                  "alg_GBps": rows * (3 * s_in + s_g) * V / (ms_r * 1e-3) / 1e9,
+                                  "entry": "aal_grpo_fwd_bwd", "groups": N // m_, "m": m_}
+            del zd, zt, zref
         del inp
         torch.cuda.empty_cache()
         sim = make_config("c5", seed=0, device=dev)

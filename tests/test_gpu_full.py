@@ -217,3 +217,44 @@ def test_c2_rows_as_sequences_and_kl_objectives(A):
     _run_general(A, zd, zt, O.LAYOUT_WINDOWS, N, K, K, (0.0, 0.0, 1.0, 1.0), idx)
     del d, zd, zt
     _free()
+
+
+# ------------------------------------------------- GRPO on the acceptance length (aal_grpo_fwd_bwd)
+def test_c2_rows_as_grpo_groups(A):
+    """The c2 rows as 256 groups of m=8 windows (the call bench.py times);
+    the reference policy's logits are the draft's plus seeded noise.  Groups
+    are independent, so the oracle recomputes sampled groups alone; the loss
+    must equal the mean over groups of the clipped surrogate evaluated from
+    the returned advantages and log-ratios."""
+    from paper_2609_24150_amd.inputs import make_config
+    d = make_config("c2", device="cuda")
+    zd, zt = d["z_draft"], d["z_target"]
+    N, K, V = zd.shape
+    m = 8
+    n_groups = N // m
+    g = torch.Generator(device=zd.device).manual_seed(11)
+    zref = (zd.float() + 0.5 * torch.randn(zd.shape, generator=g, device=zd.device)).to(zd.dtype)
+    shp = (n_groups, m * K, V)
+    zth, zrf, ztg = zd.view(shp), zref.view(shp), zt.view(shp)
+    eps_clip = 0.2
+    r = A.aal_grpo_fwd_bwd(zth, zrf, ztg, m, K, eps_clip=eps_clip)
+    torch.cuda.synchronize()
+    lr, adv = host64(r["log_rho"]), host64(r["advantage"])
+    rho = np.exp(lr)
+    sur = np.minimum(rho * adv, np.clip(rho, 1 - eps_clip, 1 + eps_clip) * adv)
+    assert rel_err(r["loss"].item(), -sur.mean()) <= 1e-5
+    for gi in _sample(n_groups, 3, seed=9):
+        o = O.grpo_loss(host64(zth[gi]), host64(zrf[gi]), host64(ztg[gi]), 1.0, O.LAYOUT_WINDOWS, 1, m * K, m, K,
+                        eps_clip=eps_clip)
+        assert np.array_equal(r["tau_theta"][gi].cpu().numpy(), o["tau_theta"][0])
+        assert np.array_equal(r["tau_ref"][gi].cpu().numpy(), o["tau_ref"][0])
+        np.testing.assert_allclose(lr[gi], o["log_rho"][0], rtol=1e-4, atol=1e-4)
+        np.testing.assert_allclose(adv[gi], o["adv"][0], rtol=1e-5, atol=1e-5)
+        near = np.abs(o["rho"][0] - (1 - eps_clip)) <= 1e-4
+        near |= np.abs(o["rho"][0] - (1 + eps_clip)) <= 1e-4
+        if near.any():
+            continue
+        coef = np.repeat(np.abs(o["coef"][0]) / K, K) / n_groups
+        check_grad(host64(r["grad"][gi]), o["grad"] / n_groups, coef, zd.dtype, zd.dtype)
+    del d, zd, zt, zref, r
+    _free()
