@@ -20,7 +20,13 @@ Readings of places where the paper is silent (each is listed in the design doc):
 * the loss is normalised by the number of windows (the window-start set W);
 * the simulated-acceptance draft token is the inverse-CDF sample of q with a
   uniform ``u1`` (smallest v whose cumulative mass exceeds u1), accepted iff
-  ``u2 * q(x) < p(x)``; the group standard deviation uses ``ddof`` (default 0).
+  ``u2 * q(x) < p(x)``; the group standard deviation uses ``ddof`` (default 0);
+* sliding windows count only when all K positions lie in the sequence; the
+  forward-KL anchor is normalised per position, the window-mean TV per window;
+* GRPO: the log ratio uses one temperature for both drafts; the constants the
+  paper leaves open (eps_clip, rho_min, rho_max, the advantage clip) are
+  arguments; a clip passes the derivative strictly inside its interval only,
+  and min(u, v) takes u's derivative when u <= v.
 
 Pinning: every function here is checked by ``tests/test_oracle_pins.py``
 against hand-computed cases, closed forms, identities the paper states,

@@ -122,3 +122,18 @@ def test_reference_equal_to_policy_is_zero(A):
     torch.cuda.synchronize()
     assert r["loss"].item() == 0.0 and not r["grad"].float().abs().max().item()
     assert not r["log_rho"].any() and not r["advantage"].any()
+
+
+def test_out_of_range_anchors_are_clamped(A):
+    """Anchors outside [0, S - (m-1) - K] are clamped into the sequence (the
+    documented convention): the result equals the oracle on clamped anchors."""
+    B, S, m, K = 2, 30, 4, 3
+    zth, zrf, zt = _inputs((B, S, 500), torch.float32, seed=7)
+    hi = S - (m - 1) - K
+    raw = torch.tensor([[-5, 7], [hi + 9, 2**30]], dtype=torch.int32).cuda()
+    r = A.aal_grpo_fwd_bwd(zth, zrf, zt, m, K, layout=SEQ, anchors=raw)
+    c = A.aal_grpo_fwd_bwd(zth, zrf, zt, m, K, layout=SEQ, anchors=raw.clamp(0, hi))
+    torch.cuda.synchronize()
+    for k in ("loss", "tau_theta", "tau_ref", "advantage", "log_rho", "grad"):
+        assert torch.equal(r[k], c[k]), k
+    _check(A, zth, zrf, zt, m, K, SEQ, anchors=raw.clamp(0, hi))
