@@ -143,7 +143,10 @@ def loss_call(op, inp, grad_dtype, flags=0):
     dcode = _lib.AAL_BF16 if zd.dtype == torch.bfloat16 else _lib.AAL_F32
     gcode = _lib.AAL_BF16 if grad_dtype == torch.bfloat16 else _lib.AAL_F32
     if op == "wtv":
-        Td, Tt = cfg.get("temp_draft", 1.0), cfg.get("temp_target", cfg.get("wtv_temp", 1.0))
+        if "wtv_temp" in cfg:  # a workload that runs both losses states one WTV temperature for both
+            Td = Tt = cfg["wtv_temp"]
+        else:
+            Td, Tt = cfg.get("temp_draft", 1.0), cfg.get("temp_target", 1.0)
 
         def fn():
             st = L.aal_wtv_fwd_bwd(zd.data_ptr(), zt.data_ptr(), dcode, N, K, V, Td, Tt, loss.data_ptr(),
@@ -242,6 +245,12 @@ def grpo_call(zth, zref, zt, m, K, grad_dtype):
                                 gcode, None, ws.data_ptr(), ws.numel(), stream.cuda_stream)
         _lib.check(st, "aal_grpo_fwd_bwd")
     return fn, stream
+
+
+def _free_gpu(torch):
+    import gc
+    gc.collect()
+    torch.cuda.empty_cache()
 
 
 def main():
@@ -353,6 +362,25 @@ def main():
         ms_s = _time_calls(fn_s, args.steps, args.warmup, st_s)
         also["sim_grpo_c5"] = {"ms": ms_s, "rows_per_s": rows5 / (ms_s * 1e-3),
                                "alg_GBps": rows5 * 2 * 2 * c5["V"] / (ms_s * 1e-3) / 1e9}
+        del fn_s, st_s
+        if args.workload == "c2":
+            # every other loss workload, each timed the same way (parity cases in the tests)
+            for name, op in (("c1_eal_fp32", "eal"), ("c3_eal_bf16", "eal"), ("c3_wtv_bf16_T0.7", "wtv"),
+                             ("c4_wtv_fp32_T0.5", "wtv")):
+                wl = name[:2]
+                c = CONFIGS[wl]
+                del sim
+                _free_gpu(torch)
+                sim = make_config(wl, seed=0, device=dev)
+                fn_c, st_c, _ = loss_call(op, sim, c["dtype"], args.flags)
+                ms_c = _time_calls(fn_c, args.steps, args.warmup, st_c)
+                r_c = c["N"] * c["K"]
+                s_c = 2 if c["dtype"] == torch.bfloat16 else 4
+                gbps = r_c * 3 * s_c * c["V"] / (ms_c * 1e-3) / 1e9
+                also[name] = {"ms": ms_c, "rows_per_s": r_c / (ms_c * 1e-3), "windows_per_s": c["N"] / (ms_c * 1e-3),
+                              "alg_GBps": gbps, "frac": gbps / HBM_PEAK_GBPS,
+                              "shape": f"{c['N']}x{c['K']}x{c['V']}"}
+                del fn_c
         out["also"] = also
     print(json.dumps(out))
 
