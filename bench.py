@@ -32,8 +32,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 PMC_PROFILE = os.path.join(ROOT, "profiles", "resident_wtv_c2_pmc.txt")
-KERNEL_SOURCES = ["paper_2609_24150_amd/csrc/aal_resident.hip", "paper_2609_24150_amd/csrc/aal_device.h",
-                  "paper_2609_24150_amd/csrc/aal_internal.h"]
+KERNEL_SOURCES = ["paper_2609_24150_amd/csrc/aal_resident.hip", "paper_2609_24150_amd/csrc/aal_resident_common.h",
+                  "paper_2609_24150_amd/csrc/aal_device.h", "paper_2609_24150_amd/csrc/aal_internal.h"]
 WORKLOAD_TEXT = {
     "c2": "WTV fwd+bwd: N=2048 windows x K=7 x V=128256, bf16 logits, bf16 grad, T=1.0/1.0",
     "c4": "WTV fwd+bwd: N=16384 windows x K=16 x V=32000, fp32 logits, fp32 grad, T=0.5/0.5",
@@ -212,7 +212,7 @@ def general_call(zd, zt, layout, B, S, K, weights, grad_dtype):
     def fn():
         st = L.aal_loss_fwd_bwd(zd.data_ptr(), zt.data_ptr(), None, dcode, layout, B, S, K, V, 1.0, 1.0, w,
                                 loss.data_ptr(), terms.data_ptr(), None, None, None, None, None, grad.data_ptr(),
-                                gcode, None, ws.data_ptr(), ws.numel(), stream.cuda_stream)
+                                gcode, None, 0, ws.data_ptr(), ws.numel(), stream.cuda_stream)
         _lib.check(st, "aal_loss_fwd_bwd")
     return fn, stream, R, W
 

@@ -222,6 +222,12 @@ size_t aal_loss_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32
  *           a_tv and e_tv are evaluated when wtv, kl or tv is non-zero; a_eal,
  *           e_eal and x* when eal is non-zero; otherwise they read 0 (x*: -1).
  * grad_draft, grad_dtype, grad_scale : as for aal_eal_fwd_bwd.
+ * flags   : AAL_FLAG_* bits.  By default one register-resident kernel reads each
+ *           logit once and writes the gradient once when V is a multiple of 8
+ *           (bf16) / 4 (fp32), K is in {1..8, 16} and z_target is given; other
+ *           shapes, and AAL_FLAG_STREAMING, take the multi-kernel schedule.  A
+ *           poll time-out of the resident schedule (not expected) sets the loss
+ *           to NaN.
  * workspace : at least aal_loss_workspace_bytes(layout, B, S, K) bytes.
  */
 aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const int32_t* labels,
@@ -230,8 +236,8 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
                               aal_loss_weights_t weights, float* loss, float* terms,
                               float* e_tv, float* e_eal, float* accept_tv, float* accept_eal,
                               int32_t* xstar, void* grad_draft, aal_dtype_t grad_dtype,
-                              const float* grad_scale, void* workspace, size_t workspace_bytes,
-                              void* stream);
+                              const float* grad_scale, uint32_t flags, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* Constants of the GRPO loss that the paper leaves unstated (its Eq. advantage
  * uses eps = 1e-6). */

@@ -59,7 +59,7 @@ _SIGNATURES = {
     "aal_loss_fwd_bwd": (C.c_int, [
         _vp, _vp, _vp, C.c_int, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_float, C.c_float,
         LossWeights, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
-        _vp, C.c_int, _vp, _vp, C.c_size_t, _vp]),
+        _vp, C.c_int, _vp, C.c_uint32, _vp, C.c_size_t, _vp]),
     "aal_grpo_workspace_bytes": (C.c_size_t, [C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
     "aal_grpo_fwd_bwd": (C.c_int, [
         _vp, _vp, _vp, _vp, C.c_int, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,

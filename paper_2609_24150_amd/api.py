@@ -152,7 +152,8 @@ def aal_loss_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor | None, K: in
                      weights=(0.0, 0.0, 0.0, 0.0), temp_draft: float = 1.0, temp_target: float = 1.0,
                      layout: int = AAL_LAYOUT_WINDOWS, labels: torch.Tensor | None = None,
                      grad: bool = True, grad_dtype: torch.dtype | None = None,
-                     grad_scale: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None) -> dict:
+                     grad_scale: torch.Tensor | None = None, flags: int = 0, ws: torch.Tensor | None = None,
+                     stream=None) -> dict:
     """Combined objective forward + backward (weights = (wtv, eal, kl, tv)).
 
     Windows layout: logits [N, K, V] (N disjoint windows).  Sequences layout:
@@ -199,7 +200,7 @@ def aal_loss_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor | None, K: in
         float(temp_draft), float(temp_target), w, _ptr(out["loss"]), _ptr(out["terms"]),
         _ptr(out["E_tv"]) if W else None, _ptr(out["E_eal"]) if W else None,
         _ptr(out["accept_tv"]), _ptr(out["accept_eal"]), _ptr(out["xstar"]),
-        _ptr(g), _dtype_code(g.dtype) if g is not None else AAL_F32, _ptr(grad_scale),
+        _ptr(g), _dtype_code(g.dtype) if g is not None else AAL_F32, _ptr(grad_scale), int(flags),
         _ptr(ws), ws.numel(), _stream(dev, stream))
     _lib.check(st, "aal_loss_fwd_bwd")
     return out

@@ -256,7 +256,7 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
                               aal_layout_t layout, int64_t B, int32_t S, int32_t K, int32_t V, float temp_draft,
                               float temp_target, aal_loss_weights_t weights, float* loss, float* terms, float* e_tv,
                               float* e_eal, float* accept_tv, float* accept_eal, int32_t* xstar, void* grad_draft,
-                              aal_dtype_t grad_dtype, const float* grad_scale, void* workspace,
+                              aal_dtype_t grad_dtype, const float* grad_scale, uint32_t flags, void* workspace,
                               size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES)
@@ -277,6 +277,7 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
   };
   if (!finite(weights.wtv) || !finite(weights.eal) || !finite(weights.kl) || !finite(weights.tv))
     return fail(AAL_ERR_ARG, "weights must be finite");
+  if (flags & ~AAL_FLAG_STREAMING) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
   const bool need_pq = weights.wtv != 0.f || weights.tv != 0.f || weights.kl != 0.f;
   const bool need_t = need_pq || (weights.eal != 0.f && labels == nullptr);
   if (!z_draft) return fail(AAL_ERR_ARG, "z_draft must be non-NULL");
@@ -334,6 +335,14 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
   a.win_tv = reinterpret_cast<float*>(wp);
   wp += aal::align256(size_t(W) * sizeof(float));
   a.win_eal = reinterpret_cast<float*>(wp);
+  wp += aal::align256(size_t(W) * sizeof(float));
+  a.res_slots = reinterpret_cast<uint64_t*>(wp);
+  a.res_slot_bytes = aal::kGenResidentSlotBytes;
+  wp += aal::kGenResidentSlotBytes;
+  a.arow = reinterpret_cast<uint64_t*>(wp);
+  wp += aal::align256(size_t(R) * 2 * sizeof(uint64_t));
+  a.res_err = reinterpret_cast<unsigned*>(wp);
+  a.streaming = (flags & AAL_FLAG_STREAMING) != 0;
   a.stream = static_cast<hipStream_t>(stream);
   hipError_t e = aal::launch_general(a);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));

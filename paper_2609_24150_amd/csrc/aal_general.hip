@@ -403,8 +403,7 @@ hipError_t launch_typed(const GenArgs& a) {
   sp.accept_eal = a.accept_eal;
   sp.xstar = a.xstar;
   k_gen_scan<<<dim3(unsigned((a.R + kBlock - 1) / kBlock)), kBlock, 0, a.stream>>>(sp);
-  k_gen_loss<<<1, kBlock, 0, a.stream>>>(a.stats, a.win_tv, a.win_eal, a.R, a.W, a.K, a.w_wtv, a.w_eal, a.w_kl,
-                                         a.w_tv, a.loss, a.terms);
+  if (hipError_t e = launch_general_loss(a); e != hipSuccess) return e;
   if (a.grad) {
     if (a.gd == DType::kBf16) {
       if (vec) grad_launch<TI, GBf16, true, 4>(a, need_pq);
@@ -419,7 +418,21 @@ hipError_t launch_typed(const GenArgs& a) {
 
 }  // namespace
 
+hipError_t launch_general_loss(const GenArgs& a) {
+  k_gen_loss<<<1, kBlock, 0, a.stream>>>(a.stats, a.win_tv, a.win_eal, a.R, a.W, a.K, a.w_wtv, a.w_eal, a.w_kl,
+                                         a.w_tv, a.loss, a.terms);
+  return hipGetLastError();
+}
+
 hipError_t launch_general(const GenArgs& a) {
+  if (!a.streaming) {
+    bool used = false;
+    if (hipError_t e = launch_general_resident(a, &used); e != hipSuccess) return e;
+    if (used) {
+      if (hipError_t e = launch_general_loss(a); e != hipSuccess) return e;
+      return launch_general_poison(a);
+    }
+  }
   return a.in == DType::kBf16 ? launch_typed<Bf16>(a) : launch_typed<F32>(a);
 }
 

@@ -105,8 +105,13 @@ struct GenStats {
 };
 static_assert(sizeof(GenStats) == 64, "GenStats layout");
 
+// Tagged partial slots of the combined-objective resident schedule (teams *
+// members <= the co-resident workgroups; 16 words per row and member).
+constexpr size_t kGenResidentSlotBytes = size_t(2) << 20;
+
 inline size_t general_workspace_bytes(int64_t rows, int64_t windows) {
-  return align256(size_t(rows) * sizeof(GenStats)) + 2 * align256(size_t(windows) * sizeof(float));
+  return align256(size_t(rows) * sizeof(GenStats)) + 2 * align256(size_t(windows) * sizeof(float)) +
+         kGenResidentSlotBytes + align256(size_t(rows) * 2 * sizeof(uint64_t)) + 256;
 }
 
 struct GenArgs {
@@ -133,11 +138,28 @@ struct GenArgs {
   GenStats* stats;         // workspace [R]
   float* win_tv;           // workspace [W]
   float* win_eal;          // workspace [W]
+  uint64_t* res_slots;     // workspace: resident schedule's tagged partials
+  size_t res_slot_bytes;
+  uint64_t* arow;          // workspace [R][2]: tagged acceptances of sliding-window chunks
+  unsigned* res_err;       // workspace: poll time-out flag
+  bool streaming;          // force the multi-kernel schedule
   hipStream_t stream;
 };
 
-// Row pass, window scan, loss, gradient pass.  Handles every shape.
+// The combined objective: the register-resident schedule when the shape
+// allows it (V a multiple of the 16-byte vector, K in {1..8, 16}, target
+// logits given, cooperative launch), else the row pass, window scan, loss and
+// gradient pass of the streaming schedule, which handles every shape.
 hipError_t launch_general(const GenArgs& a);
+
+// Register-resident schedule of the combined objective; sets *used = false
+// (enqueuing nothing) when the shape is outside what it supports.  The loss
+// reduction and the time-out check are left to the caller.
+hipError_t launch_general_resident(const GenArgs& a, bool* used);
+hipError_t launch_general_poison(const GenArgs& a);
+// Loss reduction of the combined objective over the per-row and per-window
+// values in the workspace.
+hipError_t launch_general_loss(const GenArgs& a);
 
 // Per-row quantities of the GRPO schedule.  32 bytes.
 struct GrpoRow {

@@ -30,12 +30,11 @@
 // so the exchange stays in one L2.
 #include "aal_device.h"
 #include "aal_internal.h"
+#include "aal_resident_common.h"
 
 #include <limits.h>
 
-#include <mutex>
 #include <type_traits>
-#include <vector>
 
 namespace aal {
 namespace {
@@ -46,7 +45,6 @@ constexpr int kClearBlock = 256;
 #endif
 // 16-byte vectors of each logit tensor a thread keeps per window (K * NV).
 constexpr int kSlotBudget = AAL_SLOT_BUDGET;
-constexpr unsigned kSpinLimit = 1u << 22;  // polls (~1 us each): seconds, far above any legitimate wait
 
 struct ResParams {
   const uint8_t* zd;
@@ -66,151 +64,6 @@ struct ResParams {
   uint64_t* slots;     // [parity 2][T][K][W][8] words {value bits, tag}: 0-4 phase A, 4-5 phase B
   unsigned* err;       // [1]
 };
-
-// The operand is the whole 128-bit tuple, so the data stays in the register
-// quadruple the 16-byte loads write (unpacked copies are not kept live across
-// phases, which would double the register footprint).
-__device__ __forceinline__ void pin(u32x4& x) { asm volatile("" : "+v"(x)); }
-
-__device__ __forceinline__ u32x4 neg_inf_vec(Bf16) { return u32x4{0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u}; }
-__device__ __forceinline__ u32x4 neg_inf_vec(F32) { return u32x4{0xff800000u, 0xff800000u, 0xff800000u, 0xff800000u}; }
-
-// Buffer resources: a wave-uniform 128-bit descriptor (base, byte range) in
-// SGPRs.  Accesses take a 32-bit per-lane byte offset plus an SGPR offset,
-// so no per-access 64-bit address arithmetic is needed.  For a raw buffer the
-// per-lane offset is range-checked: a store at or past the range is dropped.
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-constexpr int kRawBufferWord3 = 0x00020000;  // gfx9 raw (untyped) dword access
-constexpr int kNontemporal = 2;
-__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), int(bytes), kRawBufferWord3);
-}
-__device__ __forceinline__ u32x4 bld16(rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kNontemporal);
-}
-// The same 16 bytes per lane, delivered straight to LDS: lane l of the wave
-// writes bytes [16 l, 16 l + 16) from `dst` (wave-uniform), no VGPRs involved.
-typedef __attribute__((address_space(3))) void lds_void_t;
-__device__ __forceinline__ void bld16_lds(rsrc_t r, void* dst, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)dst, 16, voff, soff, 0, kNontemporal);
-}
-// s_waitcnt vmcnt(0) as an instruction the compiler's wait-count tracking sees
-// (gfx9 encoding: vmcnt 0, expcnt 7, lgkmcnt 15).
-__device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-// Workgroup barrier for LDS data only.  __syncthreads() is also a release
-// fence for every LDS write, which includes staging loads still in flight, so
-// it would wait for them; the workgroup exchanges in this kernel go through
-// ordinary LDS stores (and global atomics that carry their own tags), so
-// draining the LDS queue is all a barrier needs.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
-// One vector of gradient values at per-lane byte offset `off` of a row.
-template <class TG, int E>
-__device__ __forceinline__ void store_g(rsrc_t r, uint32_t off, const float (&g)[E]) {
-  if constexpr (sizeof(typename TG::storage) == 2 && E == 8) {
-    const u32x4 w = {pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]), pack_bf16x2(g[4], g[5]),
-                     pack_bf16x2(g[6], g[7])};
-    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, kNontemporal);
-  } else if constexpr (sizeof(typename TG::storage) == 2 && E == 4) {
-    const u32x2 w = {pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])};
-    __builtin_amdgcn_raw_buffer_store_b64(w, r, off, 0, kNontemporal);
-  } else if constexpr (E == 4) {
-    const u32x4 w = {__builtin_bit_cast(uint32_t, g[0]), __builtin_bit_cast(uint32_t, g[1]),
-                     __builtin_bit_cast(uint32_t, g[2]), __builtin_bit_cast(uint32_t, g[3])};
-    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, kNontemporal);
-  } else {
-    const u32x4 w0 = {__builtin_bit_cast(uint32_t, g[0]), __builtin_bit_cast(uint32_t, g[1]),
-                      __builtin_bit_cast(uint32_t, g[2]), __builtin_bit_cast(uint32_t, g[3])};
-    const u32x4 w1 = {__builtin_bit_cast(uint32_t, g[4]), __builtin_bit_cast(uint32_t, g[5]),
-                      __builtin_bit_cast(uint32_t, g[6]), __builtin_bit_cast(uint32_t, g[7])};
-    __builtin_amdgcn_raw_buffer_store_b128(w0, r, off, 0, kNontemporal);
-    __builtin_amdgcn_raw_buffer_store_b128(w1, r, off + 16u, 0, kNontemporal);
-  }
-}
-
-// One gradient value (through the same buffer path, so it lands after an
-// earlier vector store of the same thread to the same address).
-template <class TG>
-__device__ __forceinline__ void store_one(rsrc_t r, uint32_t off, float g) {
-  if constexpr (sizeof(typename TG::storage) == 2) {
-    const __bf16 h = static_cast<__bf16>(g);
-    __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, h), r, off, 0, 0);
-  } else {
-    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, g), r, off, 0, 0);
-  }
-}
-
-template <class TI, int E>
-__device__ __forceinline__ void unpackv(const u32x4& w, float (&x)[E]) {
-  TI::unpack(make_uint4(w.x, w.y, w.z, w.w), x);
-}
-
-__device__ __forceinline__ uint64_t tagged(float v, uint32_t tag) {
-  return (uint64_t(tag) << 32) | __builtin_bit_cast(uint32_t, v);
-}
-__device__ __forceinline__ void publish(uint64_t* p, float v, uint32_t tag) {
-  __hip_atomic_store(p, tagged(v, tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t peek(const uint64_t* p) {
-  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float value_of(uint64_t x) { return __builtin_bit_cast(float, uint32_t(x)); }
-
-// Reads the N consecutive tagged words at p, waiting until all carry `tag`.
-template <int N>
-__device__ __forceinline__ void collect(const uint64_t* p, uint32_t tag, unsigned* err, float (&out)[N]) {
-  uint64_t x[N];
-#pragma unroll
-  for (int i = 0; i < N; ++i) x[i] = peek(p + i);
-  unsigned spins = 0;
-  for (;;) {
-    bool ok = true;
-#pragma unroll
-    for (int i = 0; i < N; ++i) ok = ok && uint32_t(x[i] >> 32) == tag;
-    if (ok) break;
-    if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) break;
-    if (++spins > kSpinLimit) {
-      __hip_atomic_store(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      break;
-    }
-    __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-    for (int i = 0; i < N; ++i) x[i] = peek(p + i);
-  }
-#pragma unroll
-  for (int i = 0; i < N; ++i) out[i] = value_of(x[i]);
-}
-
-// Merge (msc, s) into (m, acc): references are fl(max * sc), monotone in max.
-__device__ __forceinline__ void lse_fold(float& m, float& acc, float msc, float s) {
-  const float nm = fmaxf(m, msc);
-  if (nm != kNegInf) {
-    acc = acc * ex2(m - nm) + s * ex2(msc - nm);
-    m = nm;
-  }
-}
-// Merge (value, index, payload) keeping the larger value, then the lower
-// index; the payload (the draft logit at that index) travels with it.
-__device__ __forceinline__ void argmax_fold(float& bv, float& bi, float& bz, float v, float i, float z) {
-  if (v > bv || (v == bv && __builtin_bit_cast(int, i) < __builtin_bit_cast(int, bi))) {
-    bv = v;
-    bi = i;
-    bz = z;
-  }
-}
-
-// Wave-wide argmax of (value, index) pairs, lowest index on ties, with the
-// payload of the winning lane.  All lanes receive the result.
-__device__ __forceinline__ void wave_argmax(float& bv, float& bi, float& bz) {
-  float m[1] = {bv};
-  wave_max_n(m);
-  const int x = wave_min_i(bv == m[0] ? __builtin_bit_cast(int, bi) : INT_MAX);
-  const uint64_t own = __builtin_amdgcn_ballot_w64(bv == m[0] && __builtin_bit_cast(int, bi) == x);
-  const int src = own != 0 ? __builtin_ctzll(own) : 0;
-  bz = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bz), src));
-  bv = m[0];
-  bi = __builtin_bit_cast(float, x);
-}
 
 template <class TI, class TG, int MODE, int K, int NV, int kBlock>
 __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
@@ -676,27 +529,6 @@ __global__ void k_clear(uint64_t* p, int64_t n) {
 }
 
 // -------------------------------------------------------------- dispatch
-struct DevInfo {
-  int cus = 0;
-  bool coop = false;
-};
-
-DevInfo device_info() {
-  static std::mutex mu;
-  static std::vector<DevInfo> cache;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return {};
-  std::lock_guard<std::mutex> lk(mu);
-  if (int(cache.size()) <= dev) cache.resize(dev + 1);
-  if (cache[dev].cus == 0) {
-    int cus = 0, coop = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return {};
-    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess) return {};
-    cache[dev] = {cus, coop != 0};
-  }
-  return cache[dev];
-}
-
 // Workgroup size per mode: one 512-thread workgroup per CU, which keeps the
 // teams small (less skew at each team synchronisation) and gives the LDS
 // staging the whole 144 KiB.

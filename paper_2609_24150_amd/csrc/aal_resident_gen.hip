@@ -1,0 +1,769 @@
+// Register-resident schedule for the combined objectives (aal_loss_fwd_bwd):
+// the weighted sum of the WTV, EAL, forward-KL and window-mean TV terms over
+// disjoint windows or over sequences whose windows slide by one (Sections
+// "Window TV Loss" and "Settings"), reading each logit once and writing the
+// gradient once.
+//
+// The work items are chunks of K consecutive rows of a sequence (the windows
+// layout is the special case S = K: one chunk, one window per sequence).  A
+// chunk is split by vocabulary columns over a team of W workgroups, each
+// keeping its columns of all K rows of both tensors in VGPRs, as in the
+// EAL/WTV resident kernel:
+//
+//   phase A  per-row max / sum-exp partials of the tempered draft and target
+//            and the target's greedy token with the draft logit there as a
+//            payload; published, merged in member order (bit-identical row
+//            constants in every member).  With labels, x* is the label and
+//            both logits at it are read once per row.
+//   phase B  (WTV, TV or KL term) partial sums of min(p, q), of q over
+//            q < p, and of p (log p - log q); published, merged.
+//   scan     with windows sliding over a sequence, a row's coefficient needs
+//            the acceptances of the K-1 rows on either side: one member per
+//            team publishes the chunk's a values (tagged words, written once
+//            per call) and every member reads the neighbouring chunks'.  A
+//            chunk's neighbours are processed by the adjacent teams in the
+//            same round (the next round's first team for the last one), and
+//            publishing never waits for a neighbour, so the waits always end.
+//            Then, per row, dE/da summed over the windows that contain it,
+//            and the coefficients of g = q (m ? cA : cB) + cP p + cX 1[v=x*].
+//   phase C  gradient from the registers, refill with the team's next chunk;
+//            the entry at x* is rewritten with its cX term by the thread
+//            that stored it.
+//
+// Rows of a chunk past the end of its sequence (when K does not divide S)
+// load as zeros and store nothing.  Polls are bounded; a timeout sets the
+// error word and the loss becomes NaN.
+#include "aal_device.h"
+#include "aal_internal.h"
+#include "aal_resident_common.h"
+
+#include <limits.h>
+
+#include <type_traits>
+
+namespace aal {
+namespace {
+
+constexpr int kGenBlock = 512;
+constexpr int kGenSlotWords = 16;  // per (row, member): 0-6 phase A, 8-10 phase B
+constexpr int kGenClearBlock = 256;
+
+struct GenResParams {
+  const uint8_t* zd;
+  const uint8_t* zt;
+  const int32_t* labels;  // may be null
+  uint8_t* grad;          // may be null
+  int64_t NC;             // chunks
+  int S;                  // positions per sequence (windows layout: K)
+  int CS;                 // chunks per sequence
+  int64_t Wn;             // windows
+  int64_t R;              // rows
+  int V, ng, W, T;
+  uint32_t row_bytes, grow_bytes;
+  float scd, sct, inv_t_d;
+  const float* grad_scale;
+  float w_wtv, w_eal, w_kl, w_tv;
+  int eal;                // an EAL term
+  GenStats* stats;        // kl and tv_w of every row (for the loss reduction)
+  float* win_tv;
+  float* win_eal;
+  float* e_tv;
+  float* e_eal;
+  float* accept_tv;
+  float* accept_eal;
+  int32_t* xstar;
+  uint64_t* slots;        // [2][T][K][W][16]
+  uint64_t* arow;         // [R][2]: a_tv, a_eal, tagged
+  unsigned* err;
+};
+
+template <class TI, class TG, int K, int NV, int VAR>
+__global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
+  // VAR bits: 1 a WTV, TV or KL term (target normaliser, sum min, Q<);
+  // 2 a KL term; 4 the EAL term's x* is the target's greedy token.
+  constexpr bool PQ = (VAR & 1) != 0, KL = (VAR & 2) != 0, AM = (VAR & 4) != 0;
+  constexpr int kBlock = kGenBlock;
+  constexpr int kWaves = kBlock / kWave;
+  constexpr int E = TI::kVec;
+  constexpr int GS = sizeof(typename TG::storage);
+  constexpr int kC = AM ? 7 : 4;  // phase-A words per (row, member)
+  constexpr int kPairs = K * NV;
+  constexpr int kLdsStage = 144 * 1024;
+  constexpr int kPre = kPairs < kLdsStage / (2 * kBlock * 16) ? kPairs : kLdsStage / (2 * kBlock * 16);
+  constexpr float kLn2 = 0.693147180559945309417f;
+  static_assert(kC * K <= kBlock && 2 * K <= kWave && K * K <= kBlock, "thread-per-item steps");
+  __shared__ u32x4 sh_pre[kPre][2][kBlock];
+  __shared__ float sh_w[kWaves][K][kC];
+  __shared__ float sh_row[K][6];    // msc_d, l2s_d, msc_t, l2s_t, a_eal = q(x*), p(x*)
+  __shared__ int sh_x[K];
+  __shared__ float sh_lab[K][2];    // draft and target logits at the label
+  __shared__ float sh_b[K][3];      // a_tv, Q<, KL of the chunk's rows
+  __shared__ float sh_a[3 * K][2];  // a_tv, a_eal of rows row0 - K .. row0 + 2K - 1
+  __shared__ float sh_coef[K][7];   // cA, cB, cP scaled by 2^-l2s_d; cX; cA, cB, cP unscaled
+  __shared__ float sh_d[K][K][2];   // dE/da (WTV, EAL) of row k at place jj of a window
+
+  const int b = blockIdx.x;
+  int team, member;
+  if ((p.T & 7) == 0) {
+    const int j = b >> 3;
+    team = (j / p.W) * 8 + (b & 7);
+    member = j % p.W;
+  } else {
+    team = b / p.W;
+    member = b % p.W;
+  }
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wv = tid / kWave;
+  const bool last = member == p.W - 1;
+  constexpr bool pq = PQ;
+  const bool eal = p.eal != 0;
+  constexpr bool argmax = AM;
+  int col[NV];
+  uint32_t coff[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    col[v] = member * (kBlock * NV) + v * kBlock + tid;
+    coff[v] = uint32_t(min(col[v], p.ng - 1)) * 16u;
+  }
+  uint64_t* const slots_team = p.slots + (int64_t(team) * K * p.W) * kGenSlotWords;
+  const int64_t slot_plane = int64_t(p.T) * K * p.W * kGenSlotWords;
+
+  // Chunk c: sequence c / CS, rows row0 .. row0 + nvalid - 1 of it.
+  auto chunk = [&](int64_t c, int64_t& row0, int& j, int& nvalid) {
+    const int64_t s = c / p.CS;
+    j = int(c - s * p.CS);
+    row0 = s * p.S + int64_t(j) * K;
+    nvalid = min(K, p.S - j * K);
+  };
+
+  u32x4 rd[K][NV], rt[K][NV];
+  auto pin_all = [&]() {
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        pin(rd[k][v]);
+        pin(rt[k][v]);
+      }
+  };
+
+  int64_t c = team;
+  if (c < p.NC) {
+    int64_t row0;
+    int j, nvalid;
+    chunk(c, row0, j, nvalid);
+    const uint32_t bytes = uint32_t(nvalid) * p.row_bytes;
+    const rsrc_t bd = make_rsrc(p.zd + row0 * p.row_bytes, bytes);
+    const rsrc_t bt = make_rsrc(p.zt + row0 * p.row_bytes, bytes);
+    const int wbase = __builtin_amdgcn_readfirstlane(wv * kWave);
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int k = i / NV, v = i % NV;
+      bld16_lds(bd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
+      bld16_lds(bt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+    }
+#pragma unroll
+    for (int i = kPre; i < kPairs; ++i) {
+      const int k = i / NV, v = i % NV;
+      rd[k][v] = bld16(bd, coff[v], k * p.row_bytes);
+      rt[k][v] = bld16(bt, coff[v], k * p.row_bytes);
+    }
+    wait_vmem_all();
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int k = i / NV, v = i % NV;
+      rd[k][v] = sh_pre[i][0][tid];
+      rt[k][v] = sh_pre[i][1][tid];
+    }
+    __syncthreads();
+  }
+  uint32_t iter = 0;
+  for (; c < p.NC; c += p.T, ++iter) {
+    const int parity = iter & 1;
+    const uint32_t tagA = 2u * (iter + 1u), tagB = tagA + 1u;
+    uint64_t* const slots = slots_team + parity * slot_plane;
+    int64_t row0;
+    int j, nvalid;
+    chunk(c, row0, j, nvalid);
+
+    const int64_t cn = c + p.T;
+    const bool more = cn < p.NC;
+    int64_t nrow0 = row0;
+    int nj, nnvalid = 0;
+    if (more) chunk(cn, nrow0, nj, nnvalid);
+    const rsrc_t nd = make_rsrc(p.zd + nrow0 * p.row_bytes, uint32_t(nnvalid) * p.row_bytes);
+    const rsrc_t nt = make_rsrc(p.zt + nrow0 * p.row_bytes, uint32_t(nnvalid) * p.row_bytes);
+    const int wbase = __builtin_amdgcn_readfirstlane(wv * kWave);
+
+    // With labels, x* and the two logits there are read once per row, by
+    // the first K threads; they are needed only after merge A.
+    int lab_x = 0;
+    float lab_d = 0.f, lab_t = 0.f;
+    const bool lab_thread = eal && !argmax && tid < nvalid;
+    if (lab_thread) {
+      const int64_t r = row0 + tid;
+      lab_x = min(max(p.labels[r], 0), p.V - 1);
+      lab_d = TI::load1(p.zd + r * p.row_bytes, lab_x);
+      lab_t = TI::load1(p.zt + r * p.row_bytes, lab_x);
+    }
+
+    // ------------------------------------------------------------ phase A
+    pin_all();
+    if (last) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+        if (col[v] >= p.ng)
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            rd[k][v] = neg_inf_vec(TI{});
+            rt[k][v] = neg_inf_vec(TI{});
+          }
+    }
+    float m0[K], s0[K], m1[K], s1[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int i = k * NV + v;
+        if (i < kPre) {
+          bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
+          bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+        }
+      }
+      float xs[NV][E];
+#pragma unroll
+      for (int v = 0; v < NV; ++v) unpackv<TI, E>(rd[k][v], xs[v]);
+      float m = kNegInf;
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < E; ++e) m = fmaxf(m, xs[v][e]);
+      const float msc = m * p.scd;
+      float sum = 0.f;
+      if (m != kNegInf) {
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int e = 0; e < E; ++e) sum += ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
+      }
+      m0[k] = m == kNegInf ? kNegInf : msc;
+      s0[k] = sum;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
+      m1[k] = kNegInf;
+      s1[k] = 0.f;
+      if constexpr (PQ) {
+        float mt = kNegInf;
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+        const float mtsc = mt * p.sct;
+        float st = 0.f;
+        if (mt != kNegInf) {
+#pragma unroll
+          for (int v = 0; v < NV; ++v)
+#pragma unroll
+            for (int e = 0; e < E; ++e) st += ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+        }
+        m1[k] = mt == kNegInf ? kNegInf : mtsc;
+        s1[k] = st;
+      }
+      if constexpr (AM) {
+        float best = kNegInf, bz = kNegInf;
+        int bidx = INT_MAX;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          float xd[E];
+          pin(rd[k][v]);
+          unpackv<TI, E>(rd[k][v], xd);
+#pragma unroll
+          for (int e = 0; e < E; ++e)
+            if (xs[v][e] > best) {
+              best = xs[v][e];
+              bidx = col[v] * E + e;
+              bz = xd[e];
+            }
+        }
+        float bi = __builtin_bit_cast(float, bidx);
+        wave_argmax(best, bi, bz);
+        // wave-uniform from here: stored right away rather than kept live
+        if (lane == 0) {
+          sh_w[wv][k][4] = best;
+          sh_w[wv][k][5] = bi;
+          sh_w[wv][k][6] = bz;
+        }
+      }
+    }
+    wave_lse_n(m0, s0);
+    if constexpr (PQ) wave_lse_n(m1, s1);
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        sh_w[wv][k][0] = m0[k];
+        sh_w[wv][k][1] = s0[k];
+        sh_w[wv][k][2] = m1[k];
+        sh_w[wv][k][3] = s1[k];
+      }
+    }
+    if (lab_thread) {
+      sh_x[tid] = lab_x;
+      sh_lab[tid][0] = lab_d;
+      sh_lab[tid][1] = lab_t;
+    }
+    lds_barrier();
+    if (tid < kC * K) {
+      const int k = tid / kC, cc = tid % kC;
+      float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
+      float a4 = 0.f, a5 = 0.f, a6 = 0.f;
+      if constexpr (AM) {
+        a4 = sh_w[0][k][4];
+        a5 = sh_w[0][k][5];
+        a6 = sh_w[0][k][6];
+      }
+#pragma unroll
+      for (int i = 1; i < kWaves; ++i) {
+        lse_fold(a0, a1, sh_w[i][k][0], sh_w[i][k][1]);
+        lse_fold(a2, a3, sh_w[i][k][2], sh_w[i][k][3]);
+        if constexpr (AM) argmax_fold(a4, a5, a6, sh_w[i][k][4], sh_w[i][k][5], sh_w[i][k][6]);
+      }
+      const float val = cc == 0 ? a0 : cc == 1 ? a1 : cc == 2 ? a2 : cc == 3 ? a3 : cc == 4 ? a4 : cc == 5 ? a5 : a6;
+      publish(slots + (int64_t(k) * p.W + member) * kGenSlotWords + cc, val, tagA);
+    }
+
+    // --------------------------------------------------------- merge A
+    for (int k = wv; k < K; k += kWaves) {
+      float a0[1] = {kNegInf}, a1[1] = {0.f}, a2[1] = {kNegInf}, a3[1] = {0.f};
+      float a4 = kNegInf, a5 = __builtin_bit_cast(float, INT_MAX), a6 = kNegInf;
+      for (int jm = lane; jm < p.W; jm += kWave) {
+        float q[kC];
+        collect<kC>(slots + (int64_t(k) * p.W + jm) * kGenSlotWords, tagA, p.err, q);
+        lse_fold(a0[0], a1[0], q[0], q[1]);
+        lse_fold(a2[0], a3[0], q[2], q[3]);
+        if constexpr (AM) argmax_fold(a4, a5, a6, q[4], q[kC - 2], q[kC - 1]);
+      }
+      wave_lse_n(a0, a1);
+      if constexpr (PQ) wave_lse_n(a2, a3);
+      if constexpr (AM) wave_argmax(a4, a5, a6);
+      if (lane == 0) {
+        const float mscd = a0[0], l2sd = __log2f(a1[0]);
+        const float msct = a2[0], l2st = pq ? __log2f(a3[0]) : 0.f;
+        sh_row[k][0] = mscd;
+        sh_row[k][1] = l2sd;
+        sh_row[k][2] = msct;
+        sh_row[k][3] = l2st;
+        float aq = 0.f, px = 0.f;
+        int x = -1;
+        if (eal) {
+          float zdx, ztx;
+          if constexpr (AM) {
+            x = __builtin_bit_cast(int, a5);
+            zdx = a6;
+            ztx = a4;
+            if (x == INT_MAX) {  // no finite target logit: unspecified, stay in bounds
+              x = 0;
+              zdx = k < nvalid ? TI::load1(p.zd + (row0 + k) * int64_t(p.row_bytes), 0) : 0.f;
+              ztx = kNegInf;
+            }
+          } else {
+            x = k < nvalid ? sh_x[k] : 0;
+            zdx = k < nvalid ? sh_lab[k][0] : 0.f;
+            ztx = k < nvalid ? sh_lab[k][1] : kNegInf;
+          }
+          aq = ex2(__builtin_fmaf(zdx, p.scd, -mscd) - l2sd);
+          if (pq) px = ex2(__builtin_fmaf(ztx, p.sct, -msct) - l2st);
+        }
+        sh_x[k] = x;
+        sh_row[k][4] = aq;
+        sh_row[k][5] = px;
+      }
+    }
+    lds_barrier();
+
+    // ------------------------------------------------------------ phase B
+    if constexpr (PQ) {
+      pin_all();
+      float am[K], aq[K], ak[K];
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const float mscd = sh_row[k][0];
+        const float ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
+        float sm = 0.f, sq = 0.f, sk = 0.f;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          float xd[E], xt[E];
+          unpackv<TI, E>(rd[k][v], xd);
+          unpackv<TI, E>(rt[k][v], xt);
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            // log2 q = u - l2s_d, log2 p = t - l2s_d (as in the WTV kernel)
+            const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
+            const float t = __builtin_fmaf(xt[e], p.sct, -ct);
+            const float mn = ex2(fminf(u, t));
+            sm += mn;
+            sq += (u < t) ? mn : 0.f;
+            if constexpr (KL) {
+              const float ep = ex2(t);  // p 2^l2s_d; p = 0 contributes nothing
+              sk += (ep > 0.f) ? ep * (t - u) : 0.f;
+            }
+          }
+        }
+        am[k] = sm;
+        aq[k] = sq;
+        ak[k] = sk;
+      }
+      wave_sum_n(am);
+      wave_sum_n(aq);
+      if constexpr (KL) wave_sum_n(ak);
+      if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          sh_w[wv][k][0] = am[k];
+          sh_w[wv][k][1] = aq[k];
+          sh_w[wv][k][2] = KL ? ak[k] : 0.f;
+        }
+      }
+      lds_barrier();
+      if (tid < 3 * K) {
+        const int k = tid / 3, cc = tid % 3;
+        float r = sh_w[0][k][cc];
+#pragma unroll
+        for (int i = 1; i < kWaves; ++i) r += sh_w[i][k][cc];
+        r *= ex2(-sh_row[k][1]);
+        if (cc == 2) r *= kLn2;
+        publish(slots + (int64_t(k) * p.W + member) * kGenSlotWords + 8 + cc, r, tagB);
+      }
+      for (int k = wv; k < K; k += kWaves) {
+        float r[3] = {0.f, 0.f, 0.f};
+        for (int jm = lane; jm < p.W; jm += kWave) {
+          float q[3];
+          collect<3>(slots + (int64_t(k) * p.W + jm) * kGenSlotWords + 8, tagB, p.err, q);
+          r[0] += q[0];
+          r[1] += q[1];
+          r[2] += q[2];
+        }
+        wave_sum_n(r);
+        if (lane == 0) {
+          sh_b[k][0] = r[0];
+          sh_b[k][1] = r[1];
+          sh_b[k][2] = r[2];
+        }
+      }
+    } else if (tid < K) {
+      sh_b[tid][0] = 0.f;
+      sh_b[tid][1] = 0.f;
+      sh_b[tid][2] = 0.f;
+    }
+    lds_barrier();
+
+    // --------------------------------------------------------------- scan
+    // a values of the rows row0 - K .. row0 + 2K - 1 (own chunk in the middle)
+    if (tid < K) {
+      sh_a[K + tid][0] = sh_b[tid][0];
+      sh_a[K + tid][1] = sh_row[tid][4];
+    }
+    if (p.CS > 1) {
+      if (member == 0 && tid < nvalid) {
+        uint64_t* const ar = p.arow + (row0 + tid) * 2;
+        publish(ar, sh_b[tid][0], 1u);
+        publish(ar + 1, sh_row[tid][4], 1u);
+      }
+      if (wv == 0 && lane < 2 * K) {
+        const int o = lane < K ? lane - K : lane;  // offset from row0: -K..-1, K..2K-1
+        const int pos = j * K + o;                 // position in the sequence
+        if (pos >= 0 && pos < p.S) {
+          float q[2];
+          collect<2>(p.arow + (row0 + o) * 2, 1u, p.err, q);
+          sh_a[K + o][0] = q[0];
+          sh_a[K + o][1] = q[1];
+        }
+      }
+    }
+    lds_barrier();
+    // dE/da of row k as the jj-th row of the window that starts at position
+    // s - jj (s = the row's position), one thread per (k, jj); the thread with
+    // jj = 0 also evaluates E of the window that starts at the row.
+    if (tid < K * K) {
+      const int k = tid / K, jj = tid % K;
+      const int s = j * K + k, t = s - jj;
+      float dt = 0.f, de = 0.f;
+      if (k < nvalid && t >= 0 && t <= p.S - K) {
+        const int o0 = K + (t - j * K);  // the window's first row in sh_a
+        double ptv = 1.0, peal = 1.0, stv = 1.0, seal = 1.0, etv = 0.0, eeal = 0.0;
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+          const double xa = double(sh_a[o0 + i][0]), xe = double(sh_a[o0 + i][1]);
+          if (i < jj) {
+            ptv *= xa;
+            peal *= xe;
+          }
+        }
+#pragma unroll
+        for (int i = K - 1; i > 0; --i) {
+          const double xa = double(sh_a[o0 + i][0]), xe = double(sh_a[o0 + i][1]);
+          if (i > jj) {
+            stv = 1.0 + xa * stv;
+            seal = 1.0 + xe * seal;
+          }
+        }
+        dt = float(ptv * stv);
+        de = float(peal * seal);
+        if (jj == 0 && member == 0) {
+          double pt = 1.0, pe = 1.0;
+#pragma unroll
+          for (int q = 0; q < K; ++q) {
+            pt *= double(sh_a[o0 + q][0]);
+            pe *= double(sh_a[o0 + q][1]);
+            etv += pt;
+            eeal += pe;
+          }
+          const int64_t w = (row0 - int64_t(j) * K) / p.S * int64_t(p.S - K + 1) + t;
+          p.win_tv[w] = float(etv);
+          p.win_eal[w] = float(eeal);
+          if (p.e_tv) p.e_tv[w] = float(etv);
+          if (p.e_eal) p.e_eal[w] = float(eeal);
+        }
+      }
+      sh_d[k][jj][0] = dt;
+      sh_d[k][jj][1] = de;
+    }
+    lds_barrier();
+    if (tid < nvalid) {
+      const int k = tid;
+      const int s = j * K + k;
+      double dtv = 0.0, deal = 0.0;
+#pragma unroll
+      for (int jj = 0; jj < K; ++jj) {
+        dtv += double(sh_d[k][jj][0]);
+        deal += double(sh_d[k][jj][1]);
+      }
+      const int lo = max(0, s - K + 1), hi = min(s, p.S - K);
+      const double count = hi >= lo ? double(hi - lo + 1) : 0.0;
+      const double scale = p.grad_scale ? double(*p.grad_scale) : 1.0;
+      const double f = scale * double(p.inv_t_d);
+      const double a_tv = double(sh_b[k][0]), qlt = double(sh_b[k][1]), a_eal = double(sh_row[k][4]);
+      const double Wn = double(p.Wn);
+      const double g_tv = p.Wn > 0 ? (-double(p.w_wtv) * dtv - double(p.w_tv) * count / K) / Wn : 0.0;
+      const double g_eal = p.Wn > 0 ? -double(p.w_eal) * deal / Wn : 0.0;
+      const double g_kl = double(p.w_kl) / double(p.R);
+      const double c_tv = g_tv * f, c_eal = g_eal * a_eal * f, c_kl = g_kl * f;
+      const float cA = float(c_tv * (1.0 - qlt) - c_eal + c_kl);
+      const float cB = float(-c_tv * qlt - c_eal + c_kl);
+      const float cP = float(-c_kl);
+      const float rs = ex2(-sh_row[k][1]);
+      sh_coef[k][0] = cA * rs;
+      sh_coef[k][1] = cB * rs;
+      sh_coef[k][2] = cP * rs;
+      sh_coef[k][3] = float(c_eal);
+      sh_coef[k][4] = cA;
+      sh_coef[k][5] = cB;
+      sh_coef[k][6] = cP;
+      if (member == 0) {
+        const int64_t r = row0 + k;
+        p.stats[r].kl = sh_b[k][2];
+        p.stats[r].tv_w = float(count * (1.0 - a_tv));
+        if (p.accept_tv) p.accept_tv[r] = sh_b[k][0];
+        if (p.accept_eal) p.accept_eal[r] = sh_row[k][4];
+        if (p.xstar) p.xstar[r] = eal ? sh_x[k] : -1;
+      }
+    }
+    lds_barrier();
+
+    // ------------------------------------------------------------ phase C
+    uint8_t* const gw = p.grad ? p.grad + row0 * int64_t(p.grow_bytes) : nullptr;
+    wait_vmem_all();  // staging has landed
+    pin_all();
+#pragma unroll
+    for (int jp = 0; jp < kPairs; ++jp) {
+      const int i = (jp + kPre) % kPairs;
+      const int k = i / NV, v = i % NV;
+      const float mscd = sh_row[k][0];
+      const float ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
+      float cA = sh_coef[k][0], cB = sh_coef[k][1];
+      asm volatile("" : "+v"(cA), "+v"(cB));
+      const float cP = sh_coef[k][2];
+      const rsrc_t gr = make_rsrc(gw + k * p.grow_bytes, gw != nullptr && k < nvalid ? p.grow_bytes : 0u);
+      float xd[E], g[E];
+      unpackv<TI, E>(rd[k][v], xd);
+      if constexpr (PQ) {
+        float xt[E];
+        unpackv<TI, E>(rt[k][v], xt);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
+          const float t = __builtin_fmaf(xt[e], p.sct, -ct);
+          g[e] = ex2(u) * ((u < t) ? cA : cB);
+          if constexpr (KL) g[e] = __builtin_fmaf(cP, ex2(t), g[e]);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) g[e] = cA * ex2(__builtin_fmaf(xd[e], p.scd, -mscd));
+      }
+      store_g<TG, E>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
+      asm volatile("" ::: "memory");
+      if (i < kPre) {
+        rd[k][v] = sh_pre[i][0][tid];
+        rt[k][v] = sh_pre[i][1][tid];
+      } else {
+        rd[k][v] = bld16(nd, coff[v], k * p.row_bytes);
+        rt[k][v] = bld16(nt, coff[v], k * p.row_bytes);
+      }
+    }
+    if (eal && gw != nullptr) {
+      // the entry at x*: q (m ? cA : cB) + cP p + cX, rewritten by the thread
+      // whose vector store covered it (same thread, so it lands last)
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int xk = sh_x[k];
+        bool own = false;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) own = own || (col[v] == xk / E);
+        if (own && k < nvalid) {
+          const float qx = sh_row[k][4], px = sh_row[k][5];
+          float gx = qx * ((pq && qx < px) ? sh_coef[k][4] : sh_coef[k][5]) + sh_coef[k][3];
+          if constexpr (KL) gx = __builtin_fmaf(sh_coef[k][6], px, gx);
+          const rsrc_t gr = make_rsrc(gw + k * p.grow_bytes, p.grow_bytes);
+          store_one<TG>(gr, uint32_t(xk) * GS, gx);
+        }
+      }
+    }
+    lds_barrier();
+  }
+  wait_vmem_all();
+}
+
+__global__ void k_gen_clear(uint64_t* p, int64_t n) {
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+    p[i] = 0;
+}
+
+__global__ void k_gen_poison(const unsigned* err, float* loss) {
+  if (threadIdx.x == 0 && *err != 0u) loss[0] = __builtin_nanf("");
+}
+
+template <class TI, class TG, int K, int VAR>
+hipError_t launch_kg(const GenArgs& a, bool* used) {
+  constexpr int NV = (16 / K) > 0 ? (16 / K) : 1;
+  constexpr int E = TI::kVec;
+  constexpr int kBlock = kGenBlock;
+  auto kern = k_res_gen<TI, TG, K, NV, VAR>;
+  const DevInfo di = device_info();
+  if (!di.coop || di.cus == 0) return hipSuccess;
+  const int ng = a.V / E;
+  const int W = (ng + kBlock * NV - 1) / (kBlock * NV);
+  const int64_t row_bytes = int64_t(a.V) * (a.in == DType::kBf16 ? 2 : 4);
+  const int64_t grow_bytes = int64_t(a.V) * (a.gd == DType::kBf16 ? 2 : 4);
+  if (int64_t(K) * grow_bytes >= (int64_t(1) << 31) || int64_t(K) * row_bytes >= (int64_t(1) << 31))
+    return hipSuccess;
+  const int S = a.layout == 0 ? K : a.S;
+  const int CS = (S + K - 1) / K;
+  const int64_t NC = a.B * CS;
+  int per_cu = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kBlock, 0);
+  if (e != hipSuccess) return e;
+  int64_t T = int64_t(per_cu) * di.cus / W;
+  if (T >= 8) T -= T % 8;
+  if (T > NC) T = NC;
+  if (T < 1) return hipSuccess;
+  // a chunk waits for its neighbours' acceptances, which must come from
+  // another team
+  if (CS > 1 && T < 2) return hipSuccess;
+  auto words = [&](int64_t t) { return int64_t(2) * t * K * W * kGenSlotWords; };
+  while (T > 8 && size_t(words(T)) * 8 > a.res_slot_bytes) T -= 8;
+  if (size_t(words(T)) * 8 > a.res_slot_bytes) return hipSuccess;
+  GenResParams p{};
+  p.zd = static_cast<const uint8_t*>(a.zd);
+  p.zt = static_cast<const uint8_t*>(a.zt);
+  p.labels = a.labels;
+  p.grad = static_cast<uint8_t*>(a.grad);
+  p.NC = NC;
+  p.S = S;
+  p.CS = CS;
+  p.Wn = a.W;
+  p.R = a.R;
+  p.V = a.V;
+  p.ng = ng;
+  p.W = W;
+  p.T = int(T);
+  p.row_bytes = uint32_t(row_bytes);
+  p.grow_bytes = uint32_t(grow_bytes);
+  p.scd = a.sc_d;
+  p.sct = a.sc_t;
+  p.inv_t_d = a.inv_t_d;
+  p.grad_scale = a.grad_scale;
+  p.w_wtv = a.w_wtv;
+  p.w_eal = a.w_eal;
+  p.w_kl = a.w_kl;
+  p.w_tv = a.w_tv;
+  p.eal = a.w_eal != 0.f ? 1 : 0;
+  p.stats = a.stats;
+  p.win_tv = a.win_tv;
+  p.win_eal = a.win_eal;
+  p.e_tv = a.e_tv;
+  p.e_eal = a.e_eal;
+  p.accept_tv = a.accept_tv;
+  p.accept_eal = a.accept_eal;
+  p.xstar = a.xstar;
+  p.slots = a.res_slots;
+  p.arow = a.arow;
+  p.err = a.res_err;
+  k_gen_clear<<<64, kGenClearBlock, 0, a.stream>>>(p.slots, words(T));
+  if (CS > 1) k_gen_clear<<<256, kGenClearBlock, 0, a.stream>>>(p.arow, a.R * 2);
+  k_gen_clear<<<1, 64, 0, a.stream>>>(reinterpret_cast<uint64_t*>(p.err), 1);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  void* args[] = {&p};
+  e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(unsigned(T * W)), dim3(kBlock), args, 0,
+                                 a.stream);
+  if (e != hipSuccess) return e;
+  *used = true;
+  return hipSuccess;
+}
+
+template <class TI, class TG, int VAR>
+hipError_t launch_kl(const GenArgs& a, bool* used) {
+  switch (a.K) {
+    case 1: return launch_kg<TI, TG, 1, VAR>(a, used);
+    case 2: return launch_kg<TI, TG, 2, VAR>(a, used);
+    case 3: return launch_kg<TI, TG, 3, VAR>(a, used);
+    case 4: return launch_kg<TI, TG, 4, VAR>(a, used);
+    case 5: return launch_kg<TI, TG, 5, VAR>(a, used);
+    case 6: return launch_kg<TI, TG, 6, VAR>(a, used);
+    case 7: return launch_kg<TI, TG, 7, VAR>(a, used);
+    case 8: return launch_kg<TI, TG, 8, VAR>(a, used);
+    case 16: return launch_kg<TI, TG, 16, VAR>(a, used);
+    default: return hipSuccess;
+  }
+}
+
+template <class TI, class TG>
+hipError_t launch_tg(const GenArgs& a, bool* used) {
+  const bool pq = a.w_wtv != 0.f || a.w_tv != 0.f || a.w_kl != 0.f;
+  const bool am = a.w_eal != 0.f && a.labels == nullptr;
+  if (!pq) return am ? launch_kl<TI, TG, 4>(a, used) : hipSuccess;  // EAL with labels: streaming
+  if (a.w_kl != 0.f) return am ? launch_kl<TI, TG, 7>(a, used) : launch_kl<TI, TG, 3>(a, used);
+  return am ? launch_kl<TI, TG, 5>(a, used) : launch_kl<TI, TG, 1>(a, used);
+}
+
+template <class TI>
+hipError_t launch_ti(const GenArgs& a, bool* used) {
+  if (a.gd == DType::kF32) return launch_tg<TI, GF32>(a, used);
+  if constexpr (std::is_same_v<TI, Bf16>) return launch_tg<TI, GBf16>(a, used);
+  return hipSuccess;  // fp32 logits with a bf16 gradient: streaming schedule
+}
+
+}  // namespace
+
+hipError_t launch_general_resident(const GenArgs& a, bool* used) {
+  *used = false;
+  const int E = a.in == DType::kBf16 ? Bf16::kVec : F32::kVec;
+  if (a.V % E != 0 || a.zt == nullptr || a.res_slots == nullptr) return hipSuccess;
+  return a.in == DType::kBf16 ? launch_ti<Bf16>(a, used) : launch_ti<F32>(a, used);
+}
+
+hipError_t launch_general_poison(const GenArgs& a) {
+  k_gen_poison<<<1, 64, 0, a.stream>>>(a.res_err, a.loss);
+  return hipGetLastError();
+}
+
+}  // namespace aal

@@ -110,11 +110,11 @@ def test_loss_workspace_bytes(lib):
 
 def _loss(L, lib, **kw):
     a = dict(zd=16, zt=16, lab=None, dt=0, lay=1, B=2, S=9, K=3, V=8, Td=1.0, Tt=1.0, w=(1.0, 0.0, 0.0, 0.0),
-             loss=16, grad=None, gdt=0, ws=256, wsb=1 << 30)
+             loss=16, grad=None, gdt=0, flags=0, ws=256, wsb=1 << 30)
     a.update(kw)
     return L.aal_loss_fwd_bwd(a["zd"], a["zt"], a["lab"], a["dt"], a["lay"], a["B"], a["S"], a["K"], a["V"],
                               a["Td"], a["Tt"], lib.LossWeights(*a["w"]), a["loss"], None, None, None, None, None,
-                              None, a["grad"], a["gdt"], None, a["ws"], a["wsb"], None)
+                              None, a["grad"], a["gdt"], None, a["flags"], a["ws"], a["wsb"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -122,7 +122,7 @@ def _loss(L, lib, **kw):
     (dict(Td=0.0), 1), (dict(Tt=float("nan")), 1), (dict(w=(float("inf"), 0, 0, 0)), 1),
     (dict(zd=None), 1), (dict(zt=None), 1), (dict(zt=None, w=(0, 1.0, 0, 0)), 1), (dict(loss=None), 1),
     (dict(dt=5), 2), (dict(grad=16, gdt=7), 2), (dict(zd=20), 3), (dict(grad=40), 3),
-    (dict(ws=None), 4), (dict(ws=64), 3), (dict(wsb=1000), 4), (dict(B=1 << 30, S=4), 1),
+    (dict(ws=None), 4), (dict(ws=64), 3), (dict(wsb=1000), 4), (dict(B=1 << 30, S=4), 1), (dict(flags=2), 1),
 ])
 def test_loss_validation(lib, kw, code):
     L = lib.lib()

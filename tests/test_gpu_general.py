@@ -1,7 +1,9 @@
 """GPU parity of the combined-objective entry point (aal_loss_fwd_bwd) with
 the fp64 oracle: disjoint windows and sliding windows over sequences, every
 term alone and in the paper's combinations, both dtypes, ragged and
-multi-tile vocabularies, labels, grad_scale, and windows that do not fit.
+multi-tile vocabularies, labels, grad_scale, and windows that do not fit —
+each under both schedules (the register-resident kernel, used by default
+where the shape allows, and the multi-kernel streaming schedule).
 
 Tolerances are those of tests/parity.py; the gradient coefficient of a row
 for the elementwise bound is |coef_tv| + |coef_eal| + |coef_kl| (each term's
@@ -16,6 +18,11 @@ from parity import check_grad, host64, rel_err, KAPPA
 pytestmark = pytest.mark.gpu
 
 WIN, SEQ = 0, 1
+
+
+@pytest.fixture(params=[0, 1], ids=["resident", "streaming"])
+def flags(request):
+    return request.param  # AAL_FLAG_STREAMING = 1
 
 
 @pytest.fixture(scope="module")
@@ -36,10 +43,11 @@ def _inputs(B, S, V, dtype, seed, peaks=True):
     return zd.to(dtype).cuda(), zt.to(dtype).cuda()
 
 
-def _check(A, zd, zt, K, weights, layout, Td=1.0, Tt=1.0, labels=None, gdt=None, scale=None, pass_target=True):
+def _check(A, zd, zt, K, weights, layout, Td=1.0, Tt=1.0, labels=None, gdt=None, scale=None, pass_target=True,
+           flags=0):
     B, S, V = zd.shape
     r = A.aal_loss_fwd_bwd(zd, zt if pass_target else None, K, weights=weights, temp_draft=Td, temp_target=Tt,
-                           layout=layout, labels=labels, grad_dtype=gdt,
+                           layout=layout, labels=labels, grad_dtype=gdt, flags=flags,
                            grad_scale=None if scale is None else torch.tensor([scale], device=zd.device))
     torch.cuda.synchronize()
     zd64, zt64 = host64(zd), host64(zt)
@@ -84,58 +92,84 @@ WEIGHTS = [(1, 0, 0, 0), (0, 1, 0, 0), (0, 0, 1, 0), (0, 0, 0, 1), (0, 0.1, 1, 0
 
 @pytest.mark.parametrize("weights", WEIGHTS)
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_sequences_all_terms(A, weights, dtype):
+def test_sequences_all_terms(A, weights, dtype, flags):
     zd, zt = _inputs(3, 11, 1000, dtype, seed=1)
-    _check(A, zd, zt, 4, weights, SEQ, Td=0.8, Tt=1.2)
+    _check(A, zd, zt, 4, weights, SEQ, Td=0.8, Tt=1.2, flags=flags)
 
 
 @pytest.mark.parametrize("weights", WEIGHTS)
-def test_windows_all_terms(A, weights):
+def test_windows_all_terms(A, weights, flags):
     zd, zt = _inputs(5, 4, 3000, torch.bfloat16, seed=2)
-    _check(A, zd, zt, 4, weights, WIN)
+    _check(A, zd, zt, 4, weights, WIN, flags=flags)
 
 
-@pytest.mark.parametrize("S,K", [(7, 7), (5, 7), (1, 1), (9, 1), (40, 16)])
-def test_sequence_edges(A, S, K):
-    zd, zt = _inputs(2, S, 257, torch.float32, seed=3 + S + K)
-    _check(A, zd, zt, K, (0.7, 0.4, 1.3, 0.9), SEQ, Td=0.7, Tt=0.7)
+@pytest.mark.parametrize("S,K", [(7, 7), (5, 7), (1, 1), (9, 1), (40, 16), (23, 5), (16, 8), (17, 8)])
+@pytest.mark.parametrize("V", [256, 257])
+def test_sequence_edges(A, S, K, V, flags):
+    zd, zt = _inputs(2, S, V, torch.float32, seed=3 + S + K)
+    _check(A, zd, zt, K, (0.7, 0.4, 1.3, 0.9), SEQ, Td=0.7, Tt=0.7, flags=flags)
 
 
-@pytest.mark.parametrize("V", [1, 3, 130, 2047, 2051])
-def test_ragged_vocab(A, V):
+@pytest.mark.parametrize("V", [1, 3, 8, 130, 2047, 2051, 2056])
+def test_ragged_vocab(A, V, flags):
     zd, zt = _inputs(2, 6, V, torch.bfloat16, seed=10 + V, peaks=V > 8)
-    _check(A, zd, zt, 3, (0.7, 0.4, 1.3, 0.9), SEQ, Td=1.1, Tt=0.9)
+    _check(A, zd, zt, 3, (0.7, 0.4, 1.3, 0.9), SEQ, Td=1.1, Tt=0.9, flags=flags)
 
 
-def test_fp32_grad_from_bf16_and_scale(A):
-    zd, zt = _inputs(2, 9, 777, torch.bfloat16, seed=20)
-    _check(A, zd, zt, 3, (0.7, 0.4, 1.3, 0.9), SEQ, gdt=torch.float32, scale=3.5)
+@pytest.mark.parametrize("V", [777, 776])
+def test_fp32_grad_from_bf16_and_scale(A, V, flags):
+    zd, zt = _inputs(2, 9, V, torch.bfloat16, seed=20)
+    _check(A, zd, zt, 3, (0.7, 0.4, 1.3, 0.9), SEQ, gdt=torch.float32, scale=3.5, flags=flags)
 
 
-def test_labels_and_target_free_eal(A):
+def test_labels_and_target_free_eal(A, flags):
     zd, zt = _inputs(2, 9, 512, torch.float32, seed=21)
     g = torch.Generator(device="cpu").manual_seed(5)
     lab = torch.randint(0, 512, (2 * 9,), generator=g, dtype=torch.int32).cuda()
-    _check(A, zd, zt, 3, (0, 1, 0, 0), SEQ, labels=lab)
-    _check(A, zd, zt, 3, (0, 1, 0, 0), SEQ, labels=lab, pass_target=False)
-    _check(A, zd, zt, 3, (0.5, 0.1, 1.0, 0.3), SEQ, labels=lab)
+    _check(A, zd, zt, 3, (0, 1, 0, 0), SEQ, labels=lab, flags=flags)
+    _check(A, zd, zt, 3, (0, 1, 0, 0), SEQ, labels=lab, pass_target=False, flags=flags)
+    _check(A, zd, zt, 3, (0.5, 0.1, 1.0, 0.3), SEQ, labels=lab, flags=flags)
 
 
-def test_kl_of_identical_distributions_is_zero(A):
+def test_kl_of_identical_distributions_is_zero(A, flags):
     zd, _ = _inputs(2, 5, 300, torch.float32, seed=22)
-    r = A.aal_loss_fwd_bwd(zd, zd.clone(), 3, weights=(0, 0, 1, 1), layout=SEQ)
+    r = A.aal_loss_fwd_bwd(zd, zd.clone(), 3, weights=(0, 0, 1, 1), layout=SEQ, flags=flags)
     torch.cuda.synchronize()
     assert abs(r["terms"][2].item()) < 1e-6 and abs(r["terms"][3].item()) < 1e-6
     assert r["grad"].abs().max().item() < 1e-6
 
 
-def test_sequences_match_resident_wtv_for_single_window_sequences(A):
+def test_sequences_match_resident_wtv_for_single_window_sequences(A, flags):
     """S = K: every sequence is one window, so the combined entry point and the
     fused WTV kernel compute the same loss and gradient."""
     zd, zt = _inputs(64, 7, 4096, torch.bfloat16, seed=23)
-    r = A.aal_loss_fwd_bwd(zd, zt, 7, weights=(1, 0, 0, 0), layout=SEQ)
+    r = A.aal_loss_fwd_bwd(zd, zt, 7, weights=(1, 0, 0, 0), layout=SEQ, flags=flags)
     w = A.aal_wtv_fwd_bwd(zd, zt, 1.0, 1.0)
     torch.cuda.synchronize()
     assert rel_err(r["loss"].item(), w["loss"].item()) < 1e-5
     d = (r["grad"].float() - w["grad"].float()).abs().max().item()
     assert d <= 2 * w["grad"].float().abs().max().item() * 2 ** -8
+
+
+@pytest.mark.parametrize("weights", [(1, 0, 0, 0), (0, 0.1, 1, 0), (0.7, 0.4, 1.3, 0.9)])
+def test_many_chunks_and_members(A, weights, flags):
+    """Sequences of 150 positions (22 chunks of 7, the last of 3 rows) with a
+    vocabulary split over 4 workgroups per chunk, so that chunks outnumber the
+    teams that run together and neighbouring chunks come from the next round."""
+    zd, zt = _inputs(3, 150, 32768, torch.bfloat16, seed=30)
+    _check(A, zd, zt, 7, weights, SEQ, flags=flags)
+
+
+def test_resident_is_deterministic_and_agrees_with_streaming(A):
+    zd, zt = _inputs(2, 61, 8192, torch.bfloat16, seed=31)
+    w = (0.7, 0.4, 1.3, 0.9)
+    r1 = A.aal_loss_fwd_bwd(zd, zt, 5, weights=w, layout=SEQ)
+    r2 = A.aal_loss_fwd_bwd(zd, zt, 5, weights=w, layout=SEQ)
+    s = A.aal_loss_fwd_bwd(zd, zt, 5, weights=w, layout=SEQ, flags=1)
+    torch.cuda.synchronize()
+    for k in ("loss", "terms", "E_tv", "E_eal", "accept_tv", "accept_eal", "xstar", "grad"):
+        assert torch.equal(r1[k], r2[k]), k
+    assert rel_err(r1["loss"].item(), s["loss"].item()) < 1e-5
+    assert torch.equal(r1["xstar"], s["xstar"])
+    d = (r1["grad"].float() - s["grad"].float()).abs().max().item()
+    assert d <= 2 * s["grad"].float().abs().max().item() * 2 ** -8
