@@ -152,8 +152,8 @@ def aal_loss_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor | None, K: in
                      weights=(0.0, 0.0, 0.0, 0.0), temp_draft: float = 1.0, temp_target: float = 1.0,
                      layout: int = AAL_LAYOUT_WINDOWS, labels: torch.Tensor | None = None,
                      grad: bool = True, grad_dtype: torch.dtype | None = None,
-                     grad_scale: torch.Tensor | None = None, flags: int = 0, ws: torch.Tensor | None = None,
-                     stream=None) -> dict:
+                     grad_scale: torch.Tensor | None = None, flags: int = 0, outputs: bool = True,
+                     ws: torch.Tensor | None = None, stream=None) -> dict:
     """Combined objective forward + backward (weights = (wtv, eal, kl, tv)).
 
     Windows layout: logits [N, K, V] (N disjoint windows).  Sequences layout:
@@ -164,7 +164,8 @@ def aal_loss_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor | None, K: in
 
     Returns a dict: loss [1], terms [4] (L_WTV, L_EAL, L_KL, L_TV), E_tv [W],
     E_eal [W], accept_tv [R], accept_eal [R], xstar [R] int32, grad (the
-    logits' shape, or None)."""
+    logits' shape, or None).  With outputs=False the per-window and per-row
+    arrays are not requested (None in the dict)."""
     if z_draft.dim() != 3 or not z_draft.is_cuda or not z_draft.is_contiguous():
         raise ValueError("z_draft must be a contiguous [B, S or K, V] device tensor")
     if z_target is not None:
@@ -184,11 +185,11 @@ def aal_loss_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor | None, K: in
     out = {
         "loss": torch.empty(1, dtype=torch.float32, device=dev),
         "terms": torch.empty(4, dtype=torch.float32, device=dev),
-        "E_tv": torch.empty(W, dtype=torch.float32, device=dev),
-        "E_eal": torch.empty(W, dtype=torch.float32, device=dev),
-        "accept_tv": torch.empty(R, dtype=torch.float32, device=dev),
-        "accept_eal": torch.empty(R, dtype=torch.float32, device=dev),
-        "xstar": torch.empty(R, dtype=torch.int32, device=dev),
+        "E_tv": torch.empty(W, dtype=torch.float32, device=dev) if outputs else None,
+        "E_eal": torch.empty(W, dtype=torch.float32, device=dev) if outputs else None,
+        "accept_tv": torch.empty(R, dtype=torch.float32, device=dev) if outputs else None,
+        "accept_eal": torch.empty(R, dtype=torch.float32, device=dev) if outputs else None,
+        "xstar": torch.empty(R, dtype=torch.int32, device=dev) if outputs else None,
         "grad": torch.empty(B, S, V, dtype=grad_dtype or z_draft.dtype, device=dev) if grad else None,
     }
     if ws is None:
@@ -198,7 +199,7 @@ def aal_loss_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor | None, K: in
     st = _lib.lib().aal_loss_fwd_bwd(
         _ptr(z_draft), _ptr(z_target), _ptr(labels), _dtype_code(z_draft.dtype), int(layout), B, S, K, V,
         float(temp_draft), float(temp_target), w, _ptr(out["loss"]), _ptr(out["terms"]),
-        _ptr(out["E_tv"]) if W else None, _ptr(out["E_eal"]) if W else None,
+        _ptr(out["E_tv"]) if W and outputs else None, _ptr(out["E_eal"]) if W and outputs else None,
         _ptr(out["accept_tv"]), _ptr(out["accept_eal"]), _ptr(out["xstar"]),
         _ptr(g), _dtype_code(g.dtype) if g is not None else AAL_F32, _ptr(grad_scale), int(flags),
         _ptr(ws), ws.numel(), _stream(dev, stream))

@@ -424,6 +424,13 @@ hipError_t launch_general_loss(const GenArgs& a) {
   return hipGetLastError();
 }
 
+hipError_t launch_general_resident(const GenArgs& a, bool* used) {
+  *used = false;
+  const int E = a.in == DType::kBf16 ? Bf16::kVec : F32::kVec;
+  if (a.V % E != 0 || a.zt == nullptr || a.res_slots == nullptr) return hipSuccess;
+  return a.in == DType::kBf16 ? launch_general_resident_bf16(a, used) : launch_general_resident_f32(a, used);
+}
+
 hipError_t launch_general(const GenArgs& a) {
   if (!a.streaming) {
     bool used = false;

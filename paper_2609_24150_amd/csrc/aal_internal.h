@@ -156,6 +156,9 @@ hipError_t launch_general(const GenArgs& a);
 // (enqueuing nothing) when the shape is outside what it supports.  The loss
 // reduction and the time-out check are left to the caller.
 hipError_t launch_general_resident(const GenArgs& a, bool* used);
+hipError_t launch_general_resident_bf16(const GenArgs& a, bool* used);  // bf16 logits
+hipError_t launch_general_resident_bf16_g32(const GenArgs& a, bool* used);  // bf16 logits, fp32 gradient
+hipError_t launch_general_resident_f32(const GenArgs& a, bool* used);   // fp32 logits
 hipError_t launch_general_poison(const GenArgs& a);
 // Loss reduction of the combined objective over the per-row and per-window
 // values in the workspace.

@@ -33,6 +33,8 @@
 // Rows of a chunk past the end of its sequence (when K does not divide S)
 // load as zeros and store nothing.  Polls are bounded; a timeout sets the
 // error word and the loss becomes NaN.
+#pragma once
+
 #include "aal_device.h"
 #include "aal_internal.h"
 #include "aal_resident_common.h"
@@ -79,9 +81,11 @@ struct GenResParams {
 
 template <class TI, class TG, int K, int NV, int VAR>
 __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
-  // VAR bits: 1 a WTV, TV or KL term (target normaliser, sum min, Q<);
-  // 2 a KL term; 4 the EAL term's x* is the target's greedy token.
-  constexpr bool PQ = (VAR & 1) != 0, KL = (VAR & 2) != 0, AM = (VAR & 4) != 0;
+  // VAR bits: 1 the target's normaliser (a WTV, TV or KL term); 2 a KL term;
+  // 4 the EAL term's x* is the target's greedy token; 8 sum min(p, q) and Q<
+  // (a WTV or TV term, or the a_tv / E_tv outputs).
+  constexpr bool PQ = (VAR & 1) != 0, KL = (VAR & 2) != 0, AM = (VAR & 4) != 0, TV = (VAR & 8) != 0;
+  static_assert(PQ || !(KL || TV), "KL and TV need the target normaliser");
   constexpr int kBlock = kGenBlock;
   constexpr int kWaves = kBlock / kWave;
   constexpr int E = TI::kVec;
@@ -400,9 +404,11 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
             // log2 q = u - l2s_d, log2 p = t - l2s_d (as in the WTV kernel)
             const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
             const float t = __builtin_fmaf(xt[e], p.sct, -ct);
-            const float mn = ex2(fminf(u, t));
-            sm += mn;
-            sq += (u < t) ? mn : 0.f;
+            if constexpr (TV) {
+              const float mn = ex2(fminf(u, t));
+              sm += mn;
+              sq += (u < t) ? mn : 0.f;
+            }
             if constexpr (KL) {
               const float ep = ex2(t);  // p 2^l2s_d; p = 0 contributes nothing
               sk += (ep > 0.f) ? ep * (t - u) : 0.f;
@@ -413,14 +419,16 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         aq[k] = sq;
         ak[k] = sk;
       }
-      wave_sum_n(am);
-      wave_sum_n(aq);
+      if constexpr (TV) {
+        wave_sum_n(am);
+        wave_sum_n(aq);
+      }
       if constexpr (KL) wave_sum_n(ak);
       if (lane == 0) {
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-          sh_w[wv][k][0] = am[k];
-          sh_w[wv][k][1] = aq[k];
+          sh_w[wv][k][0] = TV ? am[k] : 0.f;
+          sh_w[wv][k][1] = TV ? aq[k] : 0.f;
           sh_w[wv][k][2] = KL ? ak[k] : 0.f;
         }
       }
@@ -593,7 +601,11 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         for (int e = 0; e < E; ++e) {
           const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
           const float t = __builtin_fmaf(xt[e], p.sct, -ct);
-          g[e] = ex2(u) * ((u < t) ? cA : cB);
+          if constexpr (TV) {
+            g[e] = ex2(u) * ((u < t) ? cA : cB);
+          } else {
+            g[e] = ex2(u) * cA;  // no mask without a TV term: cA = cB
+          }
           if constexpr (KL) g[e] = __builtin_fmaf(cP, ex2(t), g[e]);
         }
       } else {
@@ -621,7 +633,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         for (int v = 0; v < NV; ++v) own = own || (col[v] == xk / E);
         if (own && k < nvalid) {
           const float qx = sh_row[k][4], px = sh_row[k][5];
-          float gx = qx * ((pq && qx < px) ? sh_coef[k][4] : sh_coef[k][5]) + sh_coef[k][3];
+          float gx = qx * ((TV && qx < px) ? sh_coef[k][4] : sh_coef[k][5]) + sh_coef[k][3];
           if constexpr (KL) gx = __builtin_fmaf(sh_coef[k][6], px, gx);
           const rsrc_t gr = make_rsrc(gw + k * p.grow_bytes, p.grow_bytes);
           store_one<TG>(gr, uint32_t(xk) * GS, gx);
@@ -738,11 +750,15 @@ hipError_t launch_kl(const GenArgs& a, bool* used) {
 
 template <class TI, class TG>
 hipError_t launch_tg(const GenArgs& a, bool* used) {
-  const bool pq = a.w_wtv != 0.f || a.w_tv != 0.f || a.w_kl != 0.f;
+  // sum min(p, q) is needed by the WTV and TV terms and by the a_tv / E_tv
+  // outputs (which the KL term alone would otherwise leave unevaluated)
+  const bool tv = a.w_wtv != 0.f || a.w_tv != 0.f || (a.w_kl != 0.f && (a.accept_tv || a.e_tv));
+  const bool kl = a.w_kl != 0.f;
   const bool am = a.w_eal != 0.f && a.labels == nullptr;
-  if (!pq) return am ? launch_kl<TI, TG, 4>(a, used) : hipSuccess;  // EAL with labels: streaming
-  if (a.w_kl != 0.f) return am ? launch_kl<TI, TG, 7>(a, used) : launch_kl<TI, TG, 3>(a, used);
-  return am ? launch_kl<TI, TG, 5>(a, used) : launch_kl<TI, TG, 1>(a, used);
+  if (!tv && !kl) return am ? launch_kl<TI, TG, 4>(a, used) : hipSuccess;  // EAL with labels: streaming
+  if (kl && tv) return am ? launch_kl<TI, TG, 15>(a, used) : launch_kl<TI, TG, 11>(a, used);
+  if (kl) return am ? launch_kl<TI, TG, 7>(a, used) : launch_kl<TI, TG, 3>(a, used);
+  return am ? launch_kl<TI, TG, 13>(a, used) : launch_kl<TI, TG, 9>(a, used);
 }
 
 template <class TI>
@@ -753,17 +769,4 @@ hipError_t launch_ti(const GenArgs& a, bool* used) {
 }
 
 }  // namespace
-
-hipError_t launch_general_resident(const GenArgs& a, bool* used) {
-  *used = false;
-  const int E = a.in == DType::kBf16 ? Bf16::kVec : F32::kVec;
-  if (a.V % E != 0 || a.zt == nullptr || a.res_slots == nullptr) return hipSuccess;
-  return a.in == DType::kBf16 ? launch_ti<Bf16>(a, used) : launch_ti<F32>(a, used);
-}
-
-hipError_t launch_general_poison(const GenArgs& a) {
-  k_gen_poison<<<1, 64, 0, a.stream>>>(a.res_err, a.loss);
-  return hipGetLastError();
-}
-
 }  // namespace aal

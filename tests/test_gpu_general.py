@@ -160,6 +160,28 @@ def test_many_chunks_and_members(A, weights, flags):
     _check(A, zd, zt, 7, weights, SEQ, flags=flags)
 
 
+@pytest.mark.parametrize("weights", [(0, 0, 1, 0), (0, 0.1, 1, 0), (0, 0.1, 1, 0.5), (0.5, 0, 1, 0)])
+@pytest.mark.parametrize("layout,shape", [(WIN, (6, 5, 4096)), (SEQ, (2, 33, 4096))])
+def test_without_per_row_outputs(A, weights, layout, shape, flags):
+    """Loss and gradient when the per-row and per-window outputs are not
+    requested (the KL term then skips sum min(p, q) in the resident schedule)."""
+    B, S, V = shape
+    zd, zt = _inputs(B, S, V, torch.bfloat16, seed=32)
+    r = A.aal_loss_fwd_bwd(zd, zt, 5, weights=weights, layout=layout, flags=flags, outputs=False)
+    torch.cuda.synchronize()
+    o = O.combined_loss(host64(zd), host64(zt), 1.0, 1.0, weights, layout, B, S, 5)
+    assert abs(r["loss"].item() - o["loss"]) <= 1e-3 * abs(o["loss"]) + 4e-5
+    coef = np.abs(o["coef_tv"]) + np.abs(o["coef_eal"]) + np.abs(o["coef_kl"])
+    q = np.exp(O.tempered_log_softmax(host64(zd).reshape(-1, V), 1.0))
+    p = np.exp(O.tempered_log_softmax(host64(zt).reshape(-1, V), 1.0))
+    near = np.abs(q - p) <= 1e-5 * np.maximum(p, q)
+    qtie = np.max(np.where(near, q, 0.0), axis=-1)
+    rows = np.abs(o["coef_tv"]) * qtie * q.max(-1) > 0.25 * KAPPA * coef
+    tv = weights[0] or weights[3]
+    check_grad(host64(r["grad"]), o["grad"], coef, zd.dtype, r["grad"].dtype,
+               exclude_rows=rows if tv else None, exclude_elems=near if tv else None)
+
+
 def test_resident_is_deterministic_and_agrees_with_streaming(A):
     zd, zt = _inputs(2, 61, 8192, torch.bfloat16, seed=31)
     w = (0.7, 0.4, 1.3, 0.9)
