@@ -221,6 +221,52 @@ static __device__ __forceinline__ void wave_lse_n(float (&msc)[N], float (&s)[N]
   wave_sum_n(s);
 }
 
+// Transposed wave reductions of N per-lane values (N a multiple of 4): the
+// four in-row DPP butterflies leave each row's total on all 16 lanes of the
+// row; then the gfx950 cross-row swaps combine two values per instruction
+// pair.  permlane16_swap(a, b) returns [a.r0, b.r0, a.r2, b.r2] and
+// [a.r1, b.r1, a.r3, b.r3] (rows of 16 lanes), so op of the two holds a's
+// rows-0+1 and rows-2+3 totals on rows 0 and 2 and b's on rows 1 and 3;
+// permlane32_swap(x, y) returns [x.lo, y.lo] and [x.hi, y.hi].  On return the
+// total of value 4j+q is out[j] on every lane of row q (lanes 16q..16q+15).
+// About 5.5 instructions per value instead of the 10 of the broadcast form.
+template <class Op, int N>
+static __device__ __forceinline__ void wave_reduce_t(float (&x)[N], float (&out)[N / 4], Op op) {
+  static_assert(N % 4 == 0, "values in groups of four");
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(x[i], dppm<0xB1>(x[i]));   // quad_perm [1,0,3,2]
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(x[i], dppm<0x4E>(x[i]));   // quad_perm [2,3,0,1]
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(x[i], dppm<0x141>(x[i]));  // row_half_mirror
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(x[i], dppm<0x140>(x[i]));  // row_mirror
+  float h[N / 2];
+#pragma unroll
+  for (int i = 0; i < N / 2; ++i) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x[2 * i]),
+                                                    __builtin_bit_cast(unsigned, x[2 * i + 1]), false, false);
+    h[i] = op(__builtin_bit_cast(float, unsigned(r[0])), __builtin_bit_cast(float, unsigned(r[1])));
+  }
+#pragma unroll
+  for (int j = 0; j < N / 4; ++j) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, h[2 * j]),
+                                                    __builtin_bit_cast(unsigned, h[2 * j + 1]), false, false);
+    out[j] = op(__builtin_bit_cast(float, unsigned(r[0])), __builtin_bit_cast(float, unsigned(r[1])));
+  }
+}
+struct OpAdd {
+  __device__ __forceinline__ float operator()(float a, float b) const { return a + b; }
+};
+struct OpMax {
+  __device__ __forceinline__ float operator()(float a, float b) const { return fmaxf(a, b); }
+};
+// The total of value i after wave_reduce_t, as a wave-uniform value.
+template <int NQ>
+static __device__ __forceinline__ float reduced_t(const float (&out)[NQ], int i) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, out[i / 4]), 16 * (i % 4)));
+}
+
 // Integer minimum over the wave (DPP steps as above), broadcast to all lanes.
 template <int Ctrl, int RowMask = 0xF>
 static __device__ __forceinline__ int dppi(int v, int id) {

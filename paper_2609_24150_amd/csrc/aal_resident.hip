@@ -258,16 +258,58 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         z1[k] = bz;
       }
     }
-    wave_lse_n(m0, s0);
-    if constexpr (kWtv) wave_lse_n(m1, s1);
-    if (lane == 0) {
+    {
+      // (max, sum) pairs of the draft (and target) rows, reduced over the
+      // wave together: the maxima first, every lane's sum rescaled to them,
+      // then the sums; lanes 16q store the values that end on row q.
+      constexpr int NL = kWtv ? 2 * K : K;
+      constexpr int NP = (NL + 3) / 4 * 4;
+      float mm[NP], ss[NP], tmp[NP];
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        sh_w[wv][k][0] = m0[k];
-        sh_w[wv][k][1] = s0[k];
-        sh_w[wv][k][2] = m1[k];
-        sh_w[wv][k][3] = s1[k];
-        if constexpr (!kWtv) sh_w[wv][k][4] = z1[k];
+        mm[k] = m0[k];
+        ss[k] = s0[k];
+        if constexpr (kWtv) {
+          mm[K + k] = m1[k];
+          ss[K + k] = s1[k];
+        }
+      }
+#pragma unroll
+      for (int i = NL; i < NP; ++i) {
+        mm[i] = kNegInf;
+        ss[i] = 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < NP; ++i) tmp[i] = mm[i];
+      float mt[NP / 4], st[NP / 4];
+      wave_reduce_t(tmp, mt, OpMax{});
+#pragma unroll
+      for (int i = 0; i < NL; ++i) {
+        const float M = reduced_t(mt, i);
+        ss[i] = (M == kNegInf) ? 0.f : ss[i] * ex2(mm[i] - M);
+      }
+      wave_reduce_t(ss, st, OpAdd{});
+      if ((lane & 15) == 0) {
+        const int q = lane >> 4;
+#pragma unroll
+        for (int jq = 0; jq < NP / 4; ++jq) {
+          const int i = 4 * jq + q;
+          if (i < NL) {
+            const int k = i % K, c = 2 * (i / K);
+            sh_w[wv][k][c] = mt[jq];
+            sh_w[wv][k][c + 1] = st[jq];
+          }
+        }
+      }
+    }
+    if constexpr (!kWtv) {
+      if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          sh_w[wv][k][2] = m1[k];
+          sh_w[wv][k][3] = s1[k];
+          sh_w[wv][k][4] = z1[k];
+        }
       }
     }
     lds_barrier();
@@ -362,13 +404,24 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         am[k] = sm;
         aq[k] = sq;
       }
-      wave_sum_n(am);
-      wave_sum_n(aq);
-      if (lane == 0) {
+      {
+        constexpr int NP = (2 * K + 3) / 4 * 4;
+        float vv[NP], vt[NP / 4];
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-          sh_w[wv][k][0] = am[k];
-          sh_w[wv][k][1] = aq[k];
+          vv[k] = am[k];
+          vv[K + k] = aq[k];
+        }
+#pragma unroll
+        for (int i = 2 * K; i < NP; ++i) vv[i] = 0.f;
+        wave_reduce_t(vv, vt, OpAdd{});
+        if ((lane & 15) == 0) {
+          const int q = lane >> 4;
+#pragma unroll
+          for (int jq = 0; jq < NP / 4; ++jq) {
+            const int i = 4 * jq + q;
+            if (i < 2 * K) sh_w[wv][i % K][i / K] = vt[jq];
+          }
         }
       }
       lds_barrier();
