@@ -300,15 +300,54 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         }
       }
     }
-    wave_lse_n(m0, s0);
-    if constexpr (PQ) wave_lse_n(m1, s1);
-    if (lane == 0) {
+    {
+      // (max, sum) pairs of the draft (and target) rows, reduced over the wave
+      // together (transposed reduction; lanes 16q store what ends on row q)
+      constexpr int NL = PQ ? 2 * K : K;
+      constexpr int NP = (NL + 3) / 4 * 4;
+      float mm[NP], ss[NP], tmp[NP];
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        sh_w[wv][k][0] = m0[k];
-        sh_w[wv][k][1] = s0[k];
-        sh_w[wv][k][2] = m1[k];
-        sh_w[wv][k][3] = s1[k];
+        mm[k] = m0[k];
+        ss[k] = s0[k];
+        if constexpr (PQ) {
+          mm[K + k] = m1[k];
+          ss[K + k] = s1[k];
+        }
+      }
+#pragma unroll
+      for (int i = NL; i < NP; ++i) {
+        mm[i] = kNegInf;
+        ss[i] = 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < NP; ++i) tmp[i] = mm[i];
+      float mt[NP / 4], st[NP / 4];
+      wave_reduce_t(tmp, mt, OpMax{});
+#pragma unroll
+      for (int i = 0; i < NL; ++i) {
+        const float M = reduced_t(mt, i);
+        ss[i] = (M == kNegInf) ? 0.f : ss[i] * ex2(mm[i] - M);
+      }
+      wave_reduce_t(ss, st, OpAdd{});
+      if ((lane & 15) == 0) {
+        const int q = lane >> 4;
+#pragma unroll
+        for (int jq = 0; jq < NP / 4; ++jq) {
+          const int i = 4 * jq + q;
+          if (i < NL) {
+            const int k = i % K, cc = 2 * (i / K);
+            sh_w[wv][k][cc] = mt[jq];
+            sh_w[wv][k][cc + 1] = st[jq];
+          }
+        }
+      }
+      if (!PQ && lane == 0) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          sh_w[wv][k][2] = kNegInf;
+          sh_w[wv][k][3] = 0.f;
+        }
       }
     }
     if (lab_thread) {
@@ -419,17 +458,41 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         aq[k] = sq;
         ak[k] = sk;
       }
-      if constexpr (TV) {
-        wave_sum_n(am);
-        wave_sum_n(aq);
-      }
-      if constexpr (KL) wave_sum_n(ak);
-      if (lane == 0) {
+      {
+        // the present sums (TV: sum min and Q<; KL), reduced together
+        constexpr int C0 = TV ? 0 : 2;            // first component present
+        constexpr int NC = (TV ? 2 : 0) + (KL ? 1 : 0);
+        constexpr int NB = NC * K;
+        constexpr int NP = (NB + 3) / 4 * 4;
+        float vv[NP], vt[NP / 4];
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-          sh_w[wv][k][0] = TV ? am[k] : 0.f;
-          sh_w[wv][k][1] = TV ? aq[k] : 0.f;
-          sh_w[wv][k][2] = KL ? ak[k] : 0.f;
+          if constexpr (TV) {
+            vv[k] = am[k];
+            vv[K + k] = aq[k];
+          }
+          if constexpr (KL) vv[(TV ? 2 * K : 0) + k] = ak[k];
+        }
+#pragma unroll
+        for (int i = NB; i < NP; ++i) vv[i] = 0.f;
+        wave_reduce_t(vv, vt, OpAdd{});
+        if ((lane & 15) == 0) {
+          const int q = lane >> 4;
+#pragma unroll
+          for (int jq = 0; jq < NP / 4; ++jq) {
+            const int i = 4 * jq + q;
+            if (i < NB) sh_w[wv][i % K][C0 + i / K] = vt[jq];
+          }
+        }
+        if (lane == 0) {
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            if constexpr (!TV) {
+              sh_w[wv][k][0] = 0.f;
+              sh_w[wv][k][1] = 0.f;
+            }
+            if constexpr (!KL) sh_w[wv][k][2] = 0.f;
+          }
         }
       }
       lds_barrier();
