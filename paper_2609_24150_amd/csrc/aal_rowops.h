@@ -18,7 +18,7 @@ struct Groups {
   static constexpr int E = VEC ? TI::kVec : 1;
   static __device__ __forceinline__ void load(const void* base, int64_t g0, int64_t gi, float (&x)[E]) {
     if constexpr (VEC) {
-      TI::unpack(ldvec(base, g0 + gi), x);
+      TI::unpack(ldvec_nt(base, g0 + gi), x);
     } else {
       x[0] = TI::load1(base, g0 + gi);
     }

@@ -30,7 +30,7 @@ struct SimGroups {
   static __device__ __forceinline__ void load(const void* base, int64_t g0, int gi, int ng, float (&x)[E]) {
     if (gi < ng) {
       if constexpr (VEC) {
-        TI::unpack(ldvec(base, g0 + gi), x);
+        TI::unpack(ldvec_nt(base, g0 + gi), x);
       } else {
         x[0] = TI::load1(base, g0 + gi);
       }
