@@ -342,6 +342,8 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
   a.arow = reinterpret_cast<uint64_t*>(wp);
   wp += aal::align256(size_t(R) * 2 * sizeof(uint64_t));
   a.res_err = reinterpret_cast<unsigned*>(wp);
+  wp += 256;
+  a.loss_parts = reinterpret_cast<double*>(wp);
   a.streaming = (flags & AAL_FLAG_STREAMING) != 0;
   a.stream = static_cast<hipStream_t>(stream);
   hipError_t e = aal::launch_general(a);

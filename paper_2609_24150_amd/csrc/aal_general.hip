@@ -11,8 +11,9 @@
 //               dE/da summed over them (Eq. eal_generic), the window-mean TV
 //               and KL weights, and the row's gradient coefficients; the row
 //               that starts a window also writes that window's E.
-//   k_gen_loss  one workgroup: the four terms and the weighted loss in a fixed
-//               summation order.
+//   k_gen_loss_parts, k_gen_loss  the four terms and the weighted loss: 64
+//               workgroups sum contiguous slices, one workgroup adds the 64
+//               partial sums (a fixed summation order throughout).
 //   k_gen_grad  one workgroup per row: dloss/dz_draft =
 //               q (m ? cA : cB) + cP p + cX 1[v = x*].
 #include "aal_device.h"
@@ -275,17 +276,21 @@ __device__ double block_sum_d(double v, double* sh) {
   return t;
 }
 
-__global__ __launch_bounds__(kBlock) void k_gen_loss(const GenStats* __restrict__ stats, const float* __restrict__ win_tv,
-                                                     const float* __restrict__ win_eal, int64_t R, int64_t W, int K,
-                                                     float w_wtv, float w_eal, float w_kl, float w_tv,
-                                                     float* __restrict__ loss, float* __restrict__ terms) {
+// Block b sums windows and rows of its contiguous slice.
+__global__ __launch_bounds__(kBlock) void k_gen_loss_parts(const GenStats* __restrict__ stats,
+                                                           const float* __restrict__ win_tv,
+                                                           const float* __restrict__ win_eal, int64_t R, int64_t W,
+                                                           double* __restrict__ parts) {
   __shared__ double sh[kWaves];
+  const int64_t b = blockIdx.x;
+  const int64_t w0 = W * b / kGenLossParts, w1 = W * (b + 1) / kGenLossParts;
+  const int64_t r0 = R * b / kGenLossParts, r1 = R * (b + 1) / kGenLossParts;
   double etv = 0.0, eeal = 0.0, kl = 0.0, tvs = 0.0;
-  for (int64_t i = threadIdx.x; i < W; i += kBlock) {
+  for (int64_t i = w0 + threadIdx.x; i < w1; i += kBlock) {
     etv += double(win_tv[i]);
     eeal += double(win_eal[i]);
   }
-  for (int64_t i = threadIdx.x; i < R; i += kBlock) {
+  for (int64_t i = r0 + threadIdx.x; i < r1; i += kBlock) {
     kl += double(stats[i].kl);
     tvs += double(stats[i].tv_w);
   }
@@ -294,6 +299,23 @@ __global__ __launch_bounds__(kBlock) void k_gen_loss(const GenStats* __restrict_
   kl = block_sum_d(kl, sh);
   tvs = block_sum_d(tvs, sh);
   if (threadIdx.x == 0) {
+    parts[b * 4 + 0] = etv;
+    parts[b * 4 + 1] = eeal;
+    parts[b * 4 + 2] = kl;
+    parts[b * 4 + 3] = tvs;
+  }
+}
+
+__global__ void k_gen_loss(const double* __restrict__ parts, int64_t R, int64_t W, int K, float w_wtv, float w_eal,
+                           float w_kl, float w_tv, float* __restrict__ loss, float* __restrict__ terms) {
+  if (threadIdx.x == 0) {
+    double etv = 0.0, eeal = 0.0, kl = 0.0, tvs = 0.0;
+    for (int b = 0; b < kGenLossParts; ++b) {
+      etv += parts[b * 4 + 0];
+      eeal += parts[b * 4 + 1];
+      kl += parts[b * 4 + 2];
+      tvs += parts[b * 4 + 3];
+    }
     // a term whose weight is 0 is not evaluated (its inputs may not be)
     const double t0 = W > 0 && w_wtv != 0.f ? -etv / double(W) : 0.0;
     const double t1 = W > 0 && w_eal != 0.f ? -eeal / double(W) : 0.0;
@@ -419,8 +441,9 @@ hipError_t launch_typed(const GenArgs& a) {
 }  // namespace
 
 hipError_t launch_general_loss(const GenArgs& a) {
-  k_gen_loss<<<1, kBlock, 0, a.stream>>>(a.stats, a.win_tv, a.win_eal, a.R, a.W, a.K, a.w_wtv, a.w_eal, a.w_kl,
-                                         a.w_tv, a.loss, a.terms);
+  k_gen_loss_parts<<<kGenLossParts, kBlock, 0, a.stream>>>(a.stats, a.win_tv, a.win_eal, a.R, a.W, a.loss_parts);
+  k_gen_loss<<<1, 64, 0, a.stream>>>(a.loss_parts, a.R, a.W, a.K, a.w_wtv, a.w_eal, a.w_kl, a.w_tv, a.loss,
+                                     a.terms);
   return hipGetLastError();
 }
 

@@ -109,9 +109,13 @@ static_assert(sizeof(GenStats) == 64, "GenStats layout");
 // members <= the co-resident workgroups; 16 words per row and member).
 constexpr size_t kGenResidentSlotBytes = size_t(2) << 20;
 
+// Blocks of the first stage of the combined objective's loss reduction.
+constexpr int kGenLossParts = 64;
+
 inline size_t general_workspace_bytes(int64_t rows, int64_t windows) {
   return align256(size_t(rows) * sizeof(GenStats)) + 2 * align256(size_t(windows) * sizeof(float)) +
-         kGenResidentSlotBytes + align256(size_t(rows) * 2 * sizeof(uint64_t)) + 256;
+         kGenResidentSlotBytes + align256(size_t(rows) * 2 * sizeof(uint64_t)) + 256 +
+         align256(size_t(kGenLossParts) * 4 * sizeof(double));
 }
 
 struct GenArgs {
@@ -142,6 +146,7 @@ struct GenArgs {
   size_t res_slot_bytes;
   uint64_t* arow;          // workspace [R][2]: tagged acceptances of sliding-window chunks
   unsigned* res_err;       // workspace: poll time-out flag
+  double* loss_parts;      // workspace [kGenLossParts][4]: first-stage sums of the loss
   bool streaming;          // force the multi-kernel schedule
   hipStream_t stream;
 };
