@@ -738,7 +738,8 @@ hipError_t launch_kg(const GenArgs& a, bool* used) {
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kBlock, 0);
   if (e != hipSuccess) return e;
   int64_t T = int64_t(per_cu) * di.cus / W;
-  if (T >= 8) T -= T % 8;
+  // every co-resident team runs (members span XCDs unless the team count is a
+  // multiple of 8)
   if (T > NC) T = NC;
   if (T < 1) return hipSuccess;
   // a chunk waits for its neighbours' acceptances, which must come from
