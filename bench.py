@@ -327,6 +327,7 @@ def main():
         fn_e, st_e, _ = loss_call("eal", inp, gdt, args.flags)
         ms_e = _time_calls(fn_e, args.steps, args.warmup, st_e)
         also["eal_same_inputs"] = {"ms": ms_e, "rows_per_s": rows / (ms_e * 1e-3),
+                                   "windows_per_s": N / (ms_e * 1e-3),
                                    "alg_GBps": rows * (2 * s_in + s_g) * V / (ms_e * 1e-3) / 1e9}
         if args.workload == "c2":
             from paper_2609_24150_amd import _lib
@@ -349,7 +350,7 @@ def main():
             shp = (N // m_, m_ * K, V)
             fn_r, st_r = grpo_call(zd.view(shp), zref.view(shp), zt.view(shp), m_, K, gdt)
             ms_r = _time_calls(fn_r, args.steps, args.warmup, st_r)
-            also["grpo_c2_m8"] = {"ms": ms_r, "rows_per_s": rows / (ms_r * 1e-3),
+            also["grpo_c2_m8"] = {"ms": ms_r, "rows_per_s": rows / (ms_r * 1e-3), "windows_per_s": N / (ms_r * 1e-3),
                                   "alg_GBps": rows * (3 * s_in + s_g) * V / (ms_r * 1e-3) / 1e9,
                                   "entry": "aal_grpo_fwd_bwd", "groups": N // m_, "m": m_}
             del zd, zt, zref
@@ -361,6 +362,7 @@ def main():
         fn_s, st_s = sim_call(sim)
         ms_s = _time_calls(fn_s, args.steps, args.warmup, st_s)
         also["sim_grpo_c5"] = {"ms": ms_s, "rows_per_s": rows5 / (ms_s * 1e-3),
+                               "windows_per_s": c5["P"] * c5["G"] / (ms_s * 1e-3),
                                "alg_GBps": rows5 * 2 * 2 * c5["V"] / (ms_s * 1e-3) / 1e9}
         del fn_s, st_s
         if args.workload == "c2":
@@ -381,6 +383,9 @@ def main():
                               "alg_GBps": gbps, "frac": gbps / HBM_PEAK_GBPS,
                               "shape": f"{c['N']}x{c['K']}x{c['V']}"}
                 del fn_c
+        for name, leg in also.items():
+            if "alg_GBps" in leg and "frac" not in leg:
+                leg["frac"] = leg["alg_GBps"] / HBM_PEAK_GBPS
         out["also"] = also
     print(json.dumps(out))
 
