@@ -120,9 +120,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   const int lane = tid & (kWave - 1);
   const int wv = tid / kWave;
   const bool last = member == p.W - 1;
-  constexpr bool pq = PQ;
   const bool eal = p.eal != 0;
-  constexpr bool argmax = AM;
   int col[NV];
   uint32_t coff[NV];
 #pragma unroll
@@ -204,7 +202,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
     // the first K threads; they are needed only after merge A.
     int lab_x = 0;
     float lab_d = 0.f, lab_t = 0.f;
-    const bool lab_thread = eal && !argmax && tid < nvalid;
+    const bool lab_thread = eal && !AM && tid < nvalid;
     if (lab_thread) {
       const int64_t r = row0 + tid;
       lab_x = min(max(p.labels[r], 0), p.V - 1);
@@ -391,7 +389,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       if constexpr (AM) wave_argmax(a4, a5, a6);
       if (lane == 0) {
         const float mscd = a0[0], l2sd = __log2f(a1[0]);
-        const float msct = a2[0], l2st = pq ? __log2f(a3[0]) : 0.f;
+        const float msct = a2[0], l2st = PQ ? __log2f(a3[0]) : 0.f;
         sh_row[k][0] = mscd;
         sh_row[k][1] = l2sd;
         sh_row[k][2] = msct;
@@ -415,7 +413,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
             ztx = k < nvalid ? sh_lab[k][1] : kNegInf;
           }
           aq = ex2(__builtin_fmaf(zdx, p.scd, -mscd) - l2sd);
-          if (pq) px = ex2(__builtin_fmaf(ztx, p.sct, -msct) - l2st);
+          if constexpr (PQ) px = ex2(__builtin_fmaf(ztx, p.sct, -msct) - l2st);
         }
         sh_x[k] = x;
         sh_row[k][4] = aq;
