@@ -16,6 +16,7 @@
 //                  summed over the windows that contain it, times the
 //                  log-softmax Jacobian (1/T)(1[v = S^theta] - pi_theta(v)).
 #include "aal_device.h"
+#include "aal_grpo_math.h"
 #include "aal_internal.h"
 #include "aal_rowops.h"
 
@@ -146,53 +147,17 @@ __device__ __forceinline__ int64_t window_row0(const GroupParams& p, int64_t gi,
 __global__ __launch_bounds__(kBlock) void k_grpo_groups(GroupParams p) {
   const int64_t gi = int64_t(blockIdx.x) * kBlock + threadIdx.x;
   if (gi >= p.n_groups) return;
-  constexpr int kMaxM = 64;
-  double R[kMaxM], lr[kMaxM];
   const int m = p.m;
-  double mean = 0.0;
-  for (int i = 0; i < m; ++i) {
-    const int64_t r0 = window_row0(p, gi, i);
-    int tth = 0, trf = 0;
-    bool mth = true, mrf = true;
-    double acc = 0.0;
-    for (int k = 0; k < p.K; ++k) {
-      const GrpoRow& w = p.rows[r0 + k];
-      mth = mth && w.s_theta == w.xstar;
-      mrf = mrf && w.s_ref == w.xstar;
-      tth += mth ? 1 : 0;
-      trf += mrf ? 1 : 0;
-      acc += double(w.lp_theta) - double(w.lp_ref);
-    }
-    R[i] = double(tth - trf);
-    lr[i] = acc / p.K;
-    mean += R[i];
-    if (p.tau_theta) p.tau_theta[gi * m + i] = tth;
-    if (p.tau_ref) p.tau_ref[gi * m + i] = trf;
-  }
-  mean /= m;
-  double var = 0.0;
-  for (int i = 0; i < m; ++i) var += (R[i] - mean) * (R[i] - mean);
-  const double sd = sqrt(var / m);
-  const double inv_nm = 1.0 / (double(p.n_groups) * m);
-  double loss = 0.0;
-  for (int i = 0; i < m; ++i) {
-    double A = (R[i] - mean) / (sd + double(p.eps));
-    if (p.adv_clip > 0.f) A = fmin(fmax(A, -double(p.adv_clip)), double(p.adv_clip));
-    const double lrc = fmin(fmax(lr[i], -10.0), 10.0);
-    const double rho_e = exp(lrc);
-    const double rho = fmin(fmax(rho_e, double(p.rho_min)), double(p.rho_max));
-    const double lo = 1.0 - double(p.eps_clip), hi = 1.0 + double(p.eps_clip);
-    const double u = rho * A, v = fmin(fmax(rho, lo), hi) * A;
-    loss += fmin(u, v);
-    // derivative conventions: a clip passes 1 strictly inside its interval; min takes u's when u <= v
-    const double dclip = (rho > lo && rho < hi) ? 1.0 : 0.0;
-    const double dsur = (u <= v) ? A : A * dclip;
-    const bool inner = rho_e > double(p.rho_min) && rho_e < double(p.rho_max) && lr[i] > -10.0 && lr[i] < 10.0;
-    p.win_coef[gi * m + i] = float(-inv_nm * dsur * (inner ? rho_e : 0.0));
-    if (p.advantage) p.advantage[gi * m + i] = float(A);
-    if (p.log_rho) p.log_rho[gi * m + i] = float(lrc);
-  }
-  p.group_loss[gi] = float(-loss / m);
+  auto row_at = [&](int i, int k) {
+    const GrpoRow& w = p.rows[window_row0(p, gi, i) + k];
+    return GrpoRowIn{w.s_theta, w.s_ref, w.xstar, w.lp_theta, w.lp_ref};
+  };
+  p.group_loss[gi] = float(grpo_group(m, p.K, row_at, p.eps, p.adv_clip, p.eps_clip, p.rho_min, p.rho_max,
+                                      1.0 / (double(p.n_groups) * m), p.win_coef + gi * m,
+                                      p.tau_theta ? p.tau_theta + gi * m : nullptr,
+                                      p.tau_ref ? p.tau_ref + gi * m : nullptr,
+                                      p.advantage ? p.advantage + gi * m : nullptr,
+                                      p.log_rho ? p.log_rho + gi * m : nullptr));
 }
 
 __global__ __launch_bounds__(kBlock) void k_grpo_loss(const float* __restrict__ group_loss, int64_t n,
