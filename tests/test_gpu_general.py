@@ -131,6 +131,22 @@ def test_labels_and_target_free_eal(A, flags):
     _check(A, zd, zt, 3, (0.5, 0.1, 1.0, 0.3), SEQ, labels=lab, flags=flags)
 
 
+@pytest.mark.parametrize("weights", [(0, 1, 0, 0), (0, 0.1, 1, 0), (0.5, 0.3, 0, 0.2)])
+def test_labels_with_a_ragged_last_chunk(A, weights, flags):
+    """S = 10 positions in chunks of K = 3 (the last chunk holds one row), x*
+    from labels (including out-of-range ones, which are clamped)."""
+    B, S, K, V = 3, 10, 3, 1024
+    zd, zt = _inputs(B, S, V, torch.bfloat16, seed=24)
+    g = torch.Generator(device="cpu").manual_seed(6)
+    lab = torch.randint(-5, V + 5, (B * S,), generator=g, dtype=torch.int32)
+    _check(A, zd, zt, K, weights, SEQ, labels=lab.clamp(0, V - 1).cuda(), flags=flags)
+    r1 = A.aal_loss_fwd_bwd(zd, zt, K, weights=weights, layout=SEQ, labels=lab.cuda(), flags=flags)
+    r2 = A.aal_loss_fwd_bwd(zd, zt, K, weights=weights, layout=SEQ, labels=lab.clamp(0, V - 1).cuda(), flags=flags)
+    torch.cuda.synchronize()
+    for k in ("loss", "terms", "grad", "xstar"):
+        assert torch.equal(r1[k], r2[k]), k
+
+
 def test_kl_of_identical_distributions_is_zero(A, flags):
     zd, _ = _inputs(2, 5, 300, torch.float32, seed=22)
     r = A.aal_loss_fwd_bwd(zd, zd.clone(), 3, weights=(0, 0, 1, 1), layout=SEQ, flags=flags)
