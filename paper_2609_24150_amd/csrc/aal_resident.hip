@@ -187,203 +187,212 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           }
     }
     float m0[K], s0[K], m1[K], s1[K], z1[K];
+    // Phase A of rows [k0, k1): per-thread partials, wave reductions, the
+    // fixed-order merge of the waves and the publication of one component
+    // per thread.
+    auto phase_a = [&](auto k0c, auto k1c) {
+      constexpr int k0 = decltype(k0c)::value, k1 = decltype(k1c)::value, KG = k1 - k0;
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
+      for (int k = k0; k < k1; ++k) {
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int i = k * NV + v;
-        if (i < kPre) {
-          bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
-          bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+        for (int v = 0; v < NV; ++v) {
+          const int i = k * NV + v;
+          if (i < kPre) {
+            bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
+            bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+          }
         }
-      }
-      float xs[NV][E];
+        float xs[NV][E];
 #pragma unroll
-      for (int v = 0; v < NV; ++v) unpackv<TI, E>(rd[k][v], xs[v]);
-      float m = kNegInf;
-#pragma unroll
-      for (int v = 0; v < NV; ++v)
-#pragma unroll
-        for (int e = 0; e < E; ++e) m = fmaxf(m, xs[v][e]);
-      const float msc = m * p.scd;
-      float sum = 0.f;
-      if (m != kNegInf) {
+        for (int v = 0; v < NV; ++v) unpackv<TI, E>(rd[k][v], xs[v]);
+        float m = kNegInf;
 #pragma unroll
         for (int v = 0; v < NV; ++v)
 #pragma unroll
-          for (int e = 0; e < E; ++e) sum += ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
-      }
-      m0[k] = m == kNegInf ? kNegInf : msc;
-      s0[k] = sum;
-#pragma unroll
-      for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
-      if constexpr (kWtv) {
-        float mt = kNegInf;
-#pragma unroll
-        for (int v = 0; v < NV; ++v)
-#pragma unroll
-          for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
-        const float mtsc = mt * p.sct;
-        float st = 0.f;
-        if (mt != kNegInf) {
+          for (int e = 0; e < E; ++e) m = fmaxf(m, xs[v][e]);
+        const float msc = m * p.scd;
+        float sum = 0.f;
+        if (m != kNegInf) {
 #pragma unroll
           for (int v = 0; v < NV; ++v)
 #pragma unroll
-            for (int e = 0; e < E; ++e) st += ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+            for (int e = 0; e < E; ++e) sum += ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
         }
-        m1[k] = mt == kNegInf ? kNegInf : mtsc;
-        s1[k] = st;
-      } else {
-        float best = kNegInf, bz = kNegInf;
-        int bidx = INT_MAX;
+        m0[k] = m == kNegInf ? kNegInf : msc;
+        s0[k] = sum;
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          float xd[E];  // the draft logits again, for the payload (not kept from above)
-          pin(rd[k][v]);
-          unpackv<TI, E>(rd[k][v], xd);
+        for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
+        if constexpr (kWtv) {
+          float mt = kNegInf;
 #pragma unroll
-          for (int e = 0; e < E; ++e)
-            if (xs[v][e] > best) {
-              best = xs[v][e];
-              bidx = col[v] * E + e;
-              bz = xd[e];
+          for (int v = 0; v < NV; ++v)
+#pragma unroll
+            for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+          const float mtsc = mt * p.sct;
+          float st = 0.f;
+          if (mt != kNegInf) {
+#pragma unroll
+            for (int v = 0; v < NV; ++v)
+#pragma unroll
+              for (int e = 0; e < E; ++e) st += ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+          }
+          m1[k] = mt == kNegInf ? kNegInf : mtsc;
+          s1[k] = st;
+        } else {
+          float best = kNegInf, bz = kNegInf;
+          int bidx = INT_MAX;
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            float xd[E];  // the draft logits again, for the payload (not kept from above)
+            pin(rd[k][v]);
+            unpackv<TI, E>(rd[k][v], xd);
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+              if (xs[v][e] > best) {
+                best = xs[v][e];
+                bidx = col[v] * E + e;
+                bz = xd[e];
+              }
+          }
+          // reduced over the wave right away: the results are wave-uniform, so
+          // the per-lane payloads are short-lived
+          float bi = __builtin_bit_cast(float, bidx);
+          wave_argmax(best, bi, bz);
+          m1[k] = best;
+          s1[k] = bi;
+          z1[k] = bz;
+        }
+      }
+      {
+        // (max, sum) pairs of the draft (and target) rows, reduced over the
+        // wave together: the maxima first, every lane's sum rescaled to them,
+        // then the sums; lanes 16q store the values that end on row q.
+        constexpr int NL = kWtv ? 2 * KG : KG;
+        constexpr int NP = (NL + 3) / 4 * 4;
+        float mm[NP], ss[NP], tmp[NP];
+#pragma unroll
+        for (int j = 0; j < KG; ++j) {
+          mm[j] = m0[k0 + j];
+          ss[j] = s0[k0 + j];
+          if constexpr (kWtv) {
+            mm[KG + j] = m1[k0 + j];
+            ss[KG + j] = s1[k0 + j];
+          }
+        }
+#pragma unroll
+        for (int i = NL; i < NP; ++i) {
+          mm[i] = kNegInf;
+          ss[i] = 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < NP; ++i) tmp[i] = mm[i];
+        float mt[NP / 4], st[NP / 4];
+        wave_reduce_t(tmp, mt, OpMax{});
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          const float M = reduced_t(mt, i);
+          ss[i] = (M == kNegInf) ? 0.f : ss[i] * ex2(mm[i] - M);
+        }
+        wave_reduce_t(ss, st, OpAdd{});
+        if ((lane & 15) == 0) {
+          const int q = lane >> 4;
+#pragma unroll
+          for (int jq = 0; jq < NP / 4; ++jq) {
+            const int i = 4 * jq + q;
+            if (i < NL) {
+              const int k = k0 + i % KG, c = 2 * (i / KG);
+              sh_w[wv][k][c] = mt[jq];
+              sh_w[wv][k][c + 1] = st[jq];
             }
-        }
-        // reduced over the wave right away: the results are wave-uniform, so
-        // the per-lane payloads are short-lived
-        float bi = __builtin_bit_cast(float, bidx);
-        wave_argmax(best, bi, bz);
-        m1[k] = best;
-        s1[k] = bi;
-        z1[k] = bz;
-      }
-    }
-    {
-      // (max, sum) pairs of the draft (and target) rows, reduced over the
-      // wave together: the maxima first, every lane's sum rescaled to them,
-      // then the sums; lanes 16q store the values that end on row q.
-      constexpr int NL = kWtv ? 2 * K : K;
-      constexpr int NP = (NL + 3) / 4 * 4;
-      float mm[NP], ss[NP], tmp[NP];
-#pragma unroll
-      for (int k = 0; k < K; ++k) {
-        mm[k] = m0[k];
-        ss[k] = s0[k];
-        if constexpr (kWtv) {
-          mm[K + k] = m1[k];
-          ss[K + k] = s1[k];
-        }
-      }
-#pragma unroll
-      for (int i = NL; i < NP; ++i) {
-        mm[i] = kNegInf;
-        ss[i] = 0.f;
-      }
-#pragma unroll
-      for (int i = 0; i < NP; ++i) tmp[i] = mm[i];
-      float mt[NP / 4], st[NP / 4];
-      wave_reduce_t(tmp, mt, OpMax{});
-#pragma unroll
-      for (int i = 0; i < NL; ++i) {
-        const float M = reduced_t(mt, i);
-        ss[i] = (M == kNegInf) ? 0.f : ss[i] * ex2(mm[i] - M);
-      }
-      wave_reduce_t(ss, st, OpAdd{});
-      if ((lane & 15) == 0) {
-        const int q = lane >> 4;
-#pragma unroll
-        for (int jq = 0; jq < NP / 4; ++jq) {
-          const int i = 4 * jq + q;
-          if (i < NL) {
-            const int k = i % K, c = 2 * (i / K);
-            sh_w[wv][k][c] = mt[jq];
-            sh_w[wv][k][c + 1] = st[jq];
           }
         }
       }
-    }
-    if constexpr (!kWtv) {
-      if (lane == 0) {
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          sh_w[wv][k][2] = m1[k];
-          sh_w[wv][k][3] = s1[k];
-          sh_w[wv][k][4] = z1[k];
-        }
-      }
-    }
-    lds_barrier();
-    if (tid < kC * K) {  // merge the waves (fixed order), publish one component each
-      const int k = tid / kC, c = tid % kC;
-      float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
-      float a4 = kWtv ? 0.f : sh_w[0][k][kC - 1];
-#pragma unroll
-      for (int i = 1; i < kWaves; ++i) {
-        lse_fold(a0, a1, sh_w[i][k][0], sh_w[i][k][1]);
-        if constexpr (kWtv) {
-          lse_fold(a2, a3, sh_w[i][k][2], sh_w[i][k][3]);
-        } else {
-          argmax_fold(a2, a3, a4, sh_w[i][k][2], sh_w[i][k][3], sh_w[i][k][kC - 1]);
-        }
-      }
-      const float val = c == 0 ? a0 : c == 1 ? a1 : c == 2 ? a2 : c == 3 ? a3 : a4;
-      publish(slots + (int64_t(k) * p.W + member) * 8 + c, val, tagA);
-    }
-
-    // ------------------------------------------------------------ phase B
-    // Row merges: wave wv takes rows wv, wv+4, ...; lane j folds members j,
-    // j+64, ... in order, then a fixed DPP tree: every member of the team
-    // obtains bit-identical row constants.
-    for (int k = wv; k < K; k += kWaves) {
-      float a0[1] = {kNegInf}, a1[1] = {0.f}, a2[1] = {kNegInf}, a3[1], a4 = kNegInf;
-      a3[0] = kWtv ? 0.f : __builtin_bit_cast(float, INT_MAX);
-      for (int j = lane; j < p.W; j += kWave) {
-        float q[kC];
-        collect<kC>(slots + (int64_t(k) * p.W + j) * 8, tagA, p.err, q);
-        lse_fold(a0[0], a1[0], q[0], q[1]);
-        if constexpr (kWtv) {
-          lse_fold(a2[0], a3[0], q[2], q[3]);
-        } else {
-          argmax_fold(a2[0], a3[0], a4, q[2], q[3], q[kC - 1]);
-        }
-      }
-      wave_lse_n(a0, a1);
-      if constexpr (kWtv) {
-        wave_lse_n(a2, a3);
+      if constexpr (!kWtv) {
         if (lane == 0) {
-          sh_row[k][0] = a0[0];
-          sh_row[k][1] = __log2f(a1[0]);
-          sh_row[k][2] = a2[0];
-          sh_row[k][3] = __log2f(a3[0]);
-        }
-      } else {
-        wave_argmax(a2[0], a3[0], a4);
-        int x = __builtin_bit_cast(int, a3[0]);
-        if (lane == 0) {
-          float zx = a4;  // the draft logit at x, carried through the merges
-          if (x == INT_MAX) {  // no finite target logit: unspecified, stay in bounds
-            x = 0;
-            zx = TI::load1(p.zd + (w * K + k) * int64_t(p.row_bytes), 0);
+#pragma unroll
+          for (int k = k0; k < k1; ++k) {
+            sh_w[wv][k][2] = m1[k];
+            sh_w[wv][k][3] = s1[k];
+            sh_w[wv][k][4] = z1[k];
           }
-          const float l2s = __log2f(a1[0]);
-          sh_x[k] = x;
-          sh_row[k][0] = a0[0];
-          sh_row[k][1] = l2s;
-          sh_row[k][2] = ex2(__builtin_fmaf(zx, p.scd, -a0[0]) - l2s);  // a = q(x*)
         }
       }
-    }
-    lds_barrier();
+      lds_barrier();
+      if (tid < kC * KG) {  // merge the waves (fixed order), publish one component each
+        const int k = k0 + tid / kC, c = tid % kC;
+        float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
+        float a4 = kWtv ? 0.f : sh_w[0][k][kC - 1];
+#pragma unroll
+        for (int i = 1; i < kWaves; ++i) {
+          lse_fold(a0, a1, sh_w[i][k][0], sh_w[i][k][1]);
+          if constexpr (kWtv) {
+            lse_fold(a2, a3, sh_w[i][k][2], sh_w[i][k][3]);
+          } else {
+            argmax_fold(a2, a3, a4, sh_w[i][k][2], sh_w[i][k][3], sh_w[i][k][kC - 1]);
+          }
+        }
+        const float val = c == 0 ? a0 : c == 1 ? a1 : c == 2 ? a2 : c == 3 ? a3 : a4;
+        publish(slots + (int64_t(k) * p.W + member) * 8 + c, val, tagA);
+      }
+    };
 
-    if constexpr (kWtv) {
+    // Row merges of phase A for rows [k0, k1): wave wv takes rows k0 + wv,
+    // k0 + wv + kWaves, ...; lane j folds members j, j+64, ... in order, then a
+    // fixed DPP tree: every member of the team obtains bit-identical row
+    // constants.
+    auto merge_a = [&](int k0, int k1) {
+      for (int k = k0 + wv; k < k1; k += kWaves) {
+        float a0[1] = {kNegInf}, a1[1] = {0.f}, a2[1] = {kNegInf}, a3[1], a4 = kNegInf;
+        a3[0] = kWtv ? 0.f : __builtin_bit_cast(float, INT_MAX);
+        for (int j = lane; j < p.W; j += kWave) {
+          float q[kC];
+          collect<kC>(slots + (int64_t(k) * p.W + j) * 8, tagA, p.err, q);
+          lse_fold(a0[0], a1[0], q[0], q[1]);
+          if constexpr (kWtv) {
+            lse_fold(a2[0], a3[0], q[2], q[3]);
+          } else {
+            argmax_fold(a2[0], a3[0], a4, q[2], q[3], q[kC - 1]);
+          }
+        }
+        wave_lse_n(a0, a1);
+        if constexpr (kWtv) {
+          wave_lse_n(a2, a3);
+          if (lane == 0) {
+            sh_row[k][0] = a0[0];
+            sh_row[k][1] = __log2f(a1[0]);
+            sh_row[k][2] = a2[0];
+            sh_row[k][3] = __log2f(a3[0]);
+          }
+        } else {
+          wave_argmax(a2[0], a3[0], a4);
+          int x = __builtin_bit_cast(int, a3[0]);
+          if (lane == 0) {
+            float zx = a4;  // the draft logit at x, carried through the merges
+            if (x == INT_MAX) {  // no finite target logit: unspecified, stay in bounds
+              x = 0;
+              zx = TI::load1(p.zd + (w * K + k) * int64_t(p.row_bytes), 0);
+            }
+            const float l2s = __log2f(a1[0]);
+            sh_x[k] = x;
+            sh_row[k][0] = a0[0];
+            sh_row[k][1] = l2s;
+            sh_row[k][2] = ex2(__builtin_fmaf(zx, p.scd, -a0[0]) - l2s);  // a = q(x*)
+          }
+        }
+      }
+    };
+    // Phase B (WTV) of rows [k0, k1): partial sums of min(p, q) and Q<,
+    // reduced over the workgroup and published.
+    auto phase_b = [&](auto k0c, auto k1c) {
+      constexpr int k0 = decltype(k0c)::value, k1 = decltype(k1c)::value, KG = k1 - k0;
       pin_all();
-      float am[K], aq[K];
+      float am[KG], aq[KG];
       // With u = x_d sc_d - msc_d and t = x_t sc_t - (msc_t + dl), each one
       // fma, log2 q = u - l2sd and log2 p = t - l2sd for dl = l2st - l2sd, so
       // min(p, q) = 2^-l2sd 2^min(u, t) and [q < p] = [u < t]: the common
       // factor is applied once per row after the reductions.
 #pragma unroll
-      for (int k = 0; k < K; ++k) {
+      for (int k = k0; k < k1; ++k) {
         const float mscd = sh_row[k][0];
         const float ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
         float sm = 0.f, sq = 0.f;
@@ -401,38 +410,41 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
             sq += (u < t) ? mn : 0.f;
           }
         }
-        am[k] = sm;
-        aq[k] = sq;
+        am[k - k0] = sm;
+        aq[k - k0] = sq;
       }
       {
-        constexpr int NP = (2 * K + 3) / 4 * 4;
+        constexpr int NP = (2 * KG + 3) / 4 * 4;
         float vv[NP], vt[NP / 4];
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          vv[k] = am[k];
-          vv[K + k] = aq[k];
+        for (int j = 0; j < KG; ++j) {
+          vv[j] = am[j];
+          vv[KG + j] = aq[j];
         }
 #pragma unroll
-        for (int i = 2 * K; i < NP; ++i) vv[i] = 0.f;
+        for (int i = 2 * KG; i < NP; ++i) vv[i] = 0.f;
         wave_reduce_t(vv, vt, OpAdd{});
         if ((lane & 15) == 0) {
           const int q = lane >> 4;
 #pragma unroll
           for (int jq = 0; jq < NP / 4; ++jq) {
             const int i = 4 * jq + q;
-            if (i < 2 * K) sh_w[wv][i % K][i / K] = vt[jq];
+            if (i < 2 * KG) sh_w[wv][k0 + i % KG][i / KG] = vt[jq];
           }
         }
       }
       lds_barrier();
-      if (tid < 2 * K) {
-        const int k = tid >> 1, c = tid & 1;
+      if (tid < 2 * KG) {
+        const int k = k0 + (tid >> 1), c = tid & 1;
         float r = sh_w[0][k][c];
 #pragma unroll
         for (int i = 1; i < kWaves; ++i) r += sh_w[i][k][c];
         publish(slots + (int64_t(k) * p.W + member) * 8 + 4 + c, r * ex2(-sh_row[k][1]), tagB);
       }
-      for (int k = wv; k < K; k += kWaves) {
+    };
+    // Merges of phase B for rows [k0, k1), as for phase A.
+    auto merge_b = [&](int k0, int k1) {
+      for (int k = k0 + wv; k < k1; k += kWaves) {
         float r[2] = {0.f, 0.f};
         for (int j = lane; j < p.W; j += kWave) {
           float q[2];
@@ -446,6 +458,39 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           sh_coef[k][1] = r[1];  // Q<_k
         }
       }
+    };
+
+    // WTV splits the rows into two groups and pipelines the team merges: each
+    // group's partials are published as soon as they are complete, and a
+    // merge is only polled once the other group's arithmetic has given the
+    // slower members time to publish, so three of the four merges of a
+    // window overlap arithmetic and only the last one waits.  EAL has one
+    // merge per window and keeps a single group.
+    constexpr int K0 = kWtv && K > 1 ? (K + 1) / 2 : K;
+    using I0 = std::integral_constant<int, 0>;
+    using IK0 = std::integral_constant<int, K0>;
+    using IK = std::integral_constant<int, K>;
+    phase_a(I0{}, IK0{});
+    if constexpr (K0 < K) phase_a(IK0{}, IK{});
+
+    // ------------------------------------------------------------ phase B
+    if constexpr (!kWtv) {
+      merge_a(0, K);
+      lds_barrier();
+    } else if constexpr (K0 == K) {
+      merge_a(0, K);
+      lds_barrier();
+      phase_b(I0{}, IK{});
+      merge_b(0, K);
+      lds_barrier();
+    } else {
+      merge_a(0, K0);
+      lds_barrier();
+      phase_b(I0{}, IK0{});
+      merge_a(K0, K);
+      lds_barrier();
+      phase_b(IK0{}, IK{});
+      merge_b(0, K);
       lds_barrier();
     }
 
