@@ -169,10 +169,20 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     // memory-counter pattern) but read nothing.
     const rsrc_t nd = make_rsrc(p.zd + (more ? wn : w) * stride_w, more ? win_bytes : 0u);
     const rsrc_t nt = make_rsrc(p.zt + (more ? wn : w) * stride_w, more ? win_bytes : 0u);
-    // The first kPre pairs of the next window are staged row by row during
-    // phase A (LDS is free after the end-of-window barrier): issued between
-    // the rows' arithmetic, the staging loads do not stall the wave.
+    // The first kPre pairs of the next window are staged into LDS during
+    // phase A (each wave stages and later reads back only its own threads'
+    // slots, so no barrier guards the buffer between windows).
     const int wbase = __builtin_amdgcn_readfirstlane(wv * kWave);
+    auto stage_row = [&](int k) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int i = k * NV + v;
+        if (i < kPre) {
+          bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
+          bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+        }
+      }
+    };
 
     // ------------------------------------------------------------ phase A
     pin_all();
@@ -194,14 +204,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       constexpr int k0 = decltype(k0c)::value, k1 = decltype(k1c)::value, KG = k1 - k0;
 #pragma unroll
       for (int k = k0; k < k1; ++k) {
-#pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          const int i = k * NV + v;
-          if (i < kPre) {
-            bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
-            bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
-          }
-        }
+        stage_row(k);  // issued between the rows' arithmetic, the loads do not stall the wave
         float xs[NV][E];
 #pragma unroll
         for (int v = 0; v < NV; ++v) unpackv<TI, E>(rd[k][v], xs[v]);
@@ -610,7 +613,12 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         }
       }
     }
-    lds_barrier();  // sh_row / sh_coef and the staging are rewritten by the next window
+    // No barrier before the next window: a wave only reads and restages its
+    // own slice of the staging buffer (after its reads above have completed),
+    // and the next window rewrites sh_w, sh_row, sh_coef and sh_x only after
+    // the barrier that closes its first phase-A group, which every wave
+    // reaches after finishing this phase C.
+    wait_lds_all();
   }
   wait_vmem_all();  // the last (empty) staging loads retire before the workgroup ends
 }

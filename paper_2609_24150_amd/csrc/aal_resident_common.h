@@ -45,6 +45,9 @@ __device__ __forceinline__ void bld16_lds(rsrc_t r, void* dst, uint32_t voff, ui
 // s_waitcnt vmcnt(0) as an instruction the compiler's wait-count tracking sees
 // (gfx9 encoding: vmcnt 0, expcnt 7, lgkmcnt 15).
 __device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// s_waitcnt lgkmcnt(0) alone (vmcnt 63, expcnt 7): the wave's LDS reads have
+// completed.
+__device__ __forceinline__ void wait_lds_all() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 // Workgroup barrier for LDS data only.  __syncthreads() is also a release
 // fence for every LDS write, which includes staging loads still in flight, so
 // it would wait for them; the workgroup exchanges in this kernel go through
