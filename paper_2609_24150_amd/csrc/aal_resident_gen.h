@@ -100,7 +100,8 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   __shared__ float sh_w[kWaves][K][kC];
   __shared__ float sh_row[K][6];    // msc_d, l2s_d, msc_t, l2s_t, a_eal = q(x*), p(x*)
   __shared__ int sh_x[K];
-  __shared__ float sh_lab[K][2];    // draft and target logits at the label
+  __shared__ int sh_labx[2][K];     // the label, by chunk parity
+  __shared__ float sh_lab[2][K][2]; // draft and target logits at the label, by chunk parity
   __shared__ float sh_b[K][3];      // a_tv, Q<, KL of the chunk's rows
   __shared__ float sh_a[3 * K][2];  // a_tv, a_eal of rows row0 - K .. row0 + 2K - 1
   __shared__ float sh_coef[K][7];   // cA, cB, cP scaled by 2^-l2s_d; cX; cA, cB, cP unscaled
@@ -223,211 +224,225 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           }
     }
     float m0[K], s0[K], m1[K], s1[K];
+    // Phase A of rows [k0, k1): per-thread partials, wave reductions, the
+    // fixed-order merge of the waves and the publication of one component
+    // per thread.
+    auto phase_a = [&](auto k0c, auto k1c) {
+      constexpr int k0 = decltype(k0c)::value, k1 = decltype(k1c)::value, KG = k1 - k0;
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
+      for (int k = k0; k < k1; ++k) {
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int i = k * NV + v;
-        if (i < kPre) {
-          bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
-          bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+        for (int v = 0; v < NV; ++v) {
+          const int i = k * NV + v;
+          if (i < kPre) {
+            bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
+            bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+          }
         }
-      }
-      float xs[NV][E];
+        float xs[NV][E];
 #pragma unroll
-      for (int v = 0; v < NV; ++v) unpackv<TI, E>(rd[k][v], xs[v]);
-      float m = kNegInf;
-#pragma unroll
-      for (int v = 0; v < NV; ++v)
-#pragma unroll
-        for (int e = 0; e < E; ++e) m = fmaxf(m, xs[v][e]);
-      const float msc = m * p.scd;
-      float sum = 0.f;
-      if (m != kNegInf) {
+        for (int v = 0; v < NV; ++v) unpackv<TI, E>(rd[k][v], xs[v]);
+        float m = kNegInf;
 #pragma unroll
         for (int v = 0; v < NV; ++v)
 #pragma unroll
-          for (int e = 0; e < E; ++e) sum += ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
-      }
-      m0[k] = m == kNegInf ? kNegInf : msc;
-      s0[k] = sum;
-#pragma unroll
-      for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
-      m1[k] = kNegInf;
-      s1[k] = 0.f;
-      if constexpr (PQ) {
-        float mt = kNegInf;
-#pragma unroll
-        for (int v = 0; v < NV; ++v)
-#pragma unroll
-          for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
-        const float mtsc = mt * p.sct;
-        float st = 0.f;
-        if (mt != kNegInf) {
+          for (int e = 0; e < E; ++e) m = fmaxf(m, xs[v][e]);
+        const float msc = m * p.scd;
+        float sum = 0.f;
+        if (m != kNegInf) {
 #pragma unroll
           for (int v = 0; v < NV; ++v)
 #pragma unroll
-            for (int e = 0; e < E; ++e) st += ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+            for (int e = 0; e < E; ++e) sum += ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
         }
-        m1[k] = mt == kNegInf ? kNegInf : mtsc;
-        s1[k] = st;
-      }
-      if constexpr (AM) {
-        float best = kNegInf, bz = kNegInf;
-        int bidx = INT_MAX;
+        m0[k] = m == kNegInf ? kNegInf : msc;
+        s0[k] = sum;
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          float xd[E];
-          pin(rd[k][v]);
-          unpackv<TI, E>(rd[k][v], xd);
-#pragma unroll
-          for (int e = 0; e < E; ++e)
-            if (xs[v][e] > best) {
-              best = xs[v][e];
-              bidx = col[v] * E + e;
-              bz = xd[e];
-            }
-        }
-        float bi = __builtin_bit_cast(float, bidx);
-        wave_argmax(best, bi, bz);
-        // wave-uniform from here: stored right away rather than kept live
-        if (lane == 0) {
-          sh_w[wv][k][4] = best;
-          sh_w[wv][k][5] = bi;
-          sh_w[wv][k][6] = bz;
-        }
-      }
-    }
-    {
-      // (max, sum) pairs of the draft (and target) rows, reduced over the wave
-      // together (transposed reduction; lanes 16q store what ends on row q)
-      constexpr int NL = PQ ? 2 * K : K;
-      constexpr int NP = (NL + 3) / 4 * 4;
-      float mm[NP], ss[NP], tmp[NP];
-#pragma unroll
-      for (int k = 0; k < K; ++k) {
-        mm[k] = m0[k];
-        ss[k] = s0[k];
+        for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
+        m1[k] = kNegInf;
+        s1[k] = 0.f;
         if constexpr (PQ) {
-          mm[K + k] = m1[k];
-          ss[K + k] = s1[k];
+          float mt = kNegInf;
+#pragma unroll
+          for (int v = 0; v < NV; ++v)
+#pragma unroll
+            for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+          const float mtsc = mt * p.sct;
+          float st = 0.f;
+          if (mt != kNegInf) {
+#pragma unroll
+            for (int v = 0; v < NV; ++v)
+#pragma unroll
+              for (int e = 0; e < E; ++e) st += ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+          }
+          m1[k] = mt == kNegInf ? kNegInf : mtsc;
+          s1[k] = st;
         }
-      }
+        if constexpr (AM) {
+          float best = kNegInf, bz = kNegInf;
+          int bidx = INT_MAX;
 #pragma unroll
-      for (int i = NL; i < NP; ++i) {
-        mm[i] = kNegInf;
-        ss[i] = 0.f;
-      }
+          for (int v = 0; v < NV; ++v) {
+            float xd[E];
+            pin(rd[k][v]);
+            unpackv<TI, E>(rd[k][v], xd);
 #pragma unroll
-      for (int i = 0; i < NP; ++i) tmp[i] = mm[i];
-      float mt[NP / 4], st[NP / 4];
-      wave_reduce_t(tmp, mt, OpMax{});
-#pragma unroll
-      for (int i = 0; i < NL; ++i) {
-        const float M = reduced_t(mt, i);
-        ss[i] = (M == kNegInf) ? 0.f : ss[i] * ex2(mm[i] - M);
-      }
-      wave_reduce_t(ss, st, OpAdd{});
-      if ((lane & 15) == 0) {
-        const int q = lane >> 4;
-#pragma unroll
-        for (int jq = 0; jq < NP / 4; ++jq) {
-          const int i = 4 * jq + q;
-          if (i < NL) {
-            const int k = i % K, cc = 2 * (i / K);
-            sh_w[wv][k][cc] = mt[jq];
-            sh_w[wv][k][cc + 1] = st[jq];
+            for (int e = 0; e < E; ++e)
+              if (xs[v][e] > best) {
+                best = xs[v][e];
+                bidx = col[v] * E + e;
+                bz = xd[e];
+              }
+          }
+          float bi = __builtin_bit_cast(float, bidx);
+          wave_argmax(best, bi, bz);
+          // wave-uniform from here: stored right away rather than kept live
+          if (lane == 0) {
+            sh_w[wv][k][4] = best;
+            sh_w[wv][k][5] = bi;
+            sh_w[wv][k][6] = bz;
           }
         }
       }
-      if (!PQ && lane == 0) {
+      {
+        // (max, sum) pairs of the draft (and target) rows, reduced over the wave
+        // together (transposed reduction; lanes 16q store what ends on row q)
+        constexpr int NL = PQ ? 2 * KG : KG;
+        constexpr int NP = (NL + 3) / 4 * 4;
+        float mm[NP], ss[NP], tmp[NP];
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          sh_w[wv][k][2] = kNegInf;
-          sh_w[wv][k][3] = 0.f;
+        for (int jr = 0; jr < KG; ++jr) {
+          mm[jr] = m0[k0 + jr];
+          ss[jr] = s0[k0 + jr];
+          if constexpr (PQ) {
+            mm[KG + jr] = m1[k0 + jr];
+            ss[KG + jr] = s1[k0 + jr];
+          }
         }
-      }
-    }
-    if (lab_thread) {
-      sh_x[tid] = lab_x;
-      sh_lab[tid][0] = lab_d;
-      sh_lab[tid][1] = lab_t;
-    }
-    lds_barrier();
-    if (tid < kC * K) {
-      const int k = tid / kC, cc = tid % kC;
-      float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
-      float a4 = 0.f, a5 = 0.f, a6 = 0.f;
-      if constexpr (AM) {
-        a4 = sh_w[0][k][4];
-        a5 = sh_w[0][k][5];
-        a6 = sh_w[0][k][6];
-      }
 #pragma unroll
-      for (int i = 1; i < kWaves; ++i) {
-        lse_fold(a0, a1, sh_w[i][k][0], sh_w[i][k][1]);
-        lse_fold(a2, a3, sh_w[i][k][2], sh_w[i][k][3]);
-        if constexpr (AM) argmax_fold(a4, a5, a6, sh_w[i][k][4], sh_w[i][k][5], sh_w[i][k][6]);
-      }
-      const float val = cc == 0 ? a0 : cc == 1 ? a1 : cc == 2 ? a2 : cc == 3 ? a3 : cc == 4 ? a4 : cc == 5 ? a5 : a6;
-      publish(slots + (int64_t(k) * p.W + member) * kGenSlotWords + cc, val, tagA);
-    }
-
-    // --------------------------------------------------------- merge A
-    for (int k = wv; k < K; k += kWaves) {
-      float a0[1] = {kNegInf}, a1[1] = {0.f}, a2[1] = {kNegInf}, a3[1] = {0.f};
-      float a4 = kNegInf, a5 = __builtin_bit_cast(float, INT_MAX), a6 = kNegInf;
-      for (int jm = lane; jm < p.W; jm += kWave) {
-        float q[kC];
-        collect<kC>(slots + (int64_t(k) * p.W + jm) * kGenSlotWords, tagA, p.err, q);
-        lse_fold(a0[0], a1[0], q[0], q[1]);
-        lse_fold(a2[0], a3[0], q[2], q[3]);
-        if constexpr (AM) argmax_fold(a4, a5, a6, q[4], q[kC - 2], q[kC - 1]);
-      }
-      wave_lse_n(a0, a1);
-      if constexpr (PQ) wave_lse_n(a2, a3);
-      if constexpr (AM) wave_argmax(a4, a5, a6);
-      if (lane == 0) {
-        const float mscd = a0[0], l2sd = __log2f(a1[0]);
-        const float msct = a2[0], l2st = PQ ? __log2f(a3[0]) : 0.f;
-        sh_row[k][0] = mscd;
-        sh_row[k][1] = l2sd;
-        sh_row[k][2] = msct;
-        sh_row[k][3] = l2st;
-        float aq = 0.f, px = 0.f;
-        int x = -1;
-        if (eal) {
-          float zdx, ztx;
-          if constexpr (AM) {
-            x = __builtin_bit_cast(int, a5);
-            zdx = a6;
-            ztx = a4;
-            if (x == INT_MAX) {  // no finite target logit: unspecified, stay in bounds
-              x = 0;
-              zdx = k < nvalid ? TI::load1(p.zd + (row0 + k) * int64_t(p.row_bytes), 0) : 0.f;
-              ztx = kNegInf;
+        for (int i = NL; i < NP; ++i) {
+          mm[i] = kNegInf;
+          ss[i] = 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < NP; ++i) tmp[i] = mm[i];
+        float mt[NP / 4], st[NP / 4];
+        wave_reduce_t(tmp, mt, OpMax{});
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          const float M = reduced_t(mt, i);
+          ss[i] = (M == kNegInf) ? 0.f : ss[i] * ex2(mm[i] - M);
+        }
+        wave_reduce_t(ss, st, OpAdd{});
+        if ((lane & 15) == 0) {
+          const int q = lane >> 4;
+#pragma unroll
+          for (int jq = 0; jq < NP / 4; ++jq) {
+            const int i = 4 * jq + q;
+            if (i < NL) {
+              const int k = k0 + i % KG, cc = 2 * (i / KG);
+              sh_w[wv][k][cc] = mt[jq];
+              sh_w[wv][k][cc + 1] = st[jq];
             }
-          } else {
-            x = k < nvalid ? sh_x[k] : 0;
-            zdx = k < nvalid ? sh_lab[k][0] : 0.f;
-            ztx = k < nvalid ? sh_lab[k][1] : kNegInf;
           }
-          aq = ex2(__builtin_fmaf(zdx, p.scd, -mscd) - l2sd);
-          if constexpr (PQ) px = ex2(__builtin_fmaf(ztx, p.sct, -msct) - l2st);
         }
-        sh_x[k] = x;
-        sh_row[k][4] = aq;
-        sh_row[k][5] = px;
-      }
-    }
-    lds_barrier();
-
-    // ------------------------------------------------------------ phase B
-    if constexpr (PQ) {
-      pin_all();
-      float am[K], aq[K], ak[K];
+        if (!PQ && lane == 0) {
 #pragma unroll
-      for (int k = 0; k < K; ++k) {
+          for (int k = k0; k < k1; ++k) {
+            sh_w[wv][k][2] = kNegInf;
+            sh_w[wv][k][3] = 0.f;
+          }
+        }
+      }
+      if constexpr (k0 == 0) {
+        // the label data, double-buffered by parity: a slower wave may still
+        // be in the previous chunk's phase C
+        if (lab_thread) {
+          sh_labx[parity][tid] = lab_x;
+          sh_lab[parity][tid][0] = lab_d;
+          sh_lab[parity][tid][1] = lab_t;
+        }
+      }
+      lds_barrier();
+      if (tid < kC * KG) {
+        const int k = k0 + tid / kC, cc = tid % kC;
+        float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
+        float a4 = 0.f, a5 = 0.f, a6 = 0.f;
+        if constexpr (AM) {
+          a4 = sh_w[0][k][4];
+          a5 = sh_w[0][k][5];
+          a6 = sh_w[0][k][6];
+        }
+#pragma unroll
+        for (int i = 1; i < kWaves; ++i) {
+          lse_fold(a0, a1, sh_w[i][k][0], sh_w[i][k][1]);
+          lse_fold(a2, a3, sh_w[i][k][2], sh_w[i][k][3]);
+          if constexpr (AM) argmax_fold(a4, a5, a6, sh_w[i][k][4], sh_w[i][k][5], sh_w[i][k][6]);
+        }
+        const float val = cc == 0 ? a0 : cc == 1 ? a1 : cc == 2 ? a2 : cc == 3 ? a3 : cc == 4 ? a4 : cc == 5 ? a5 : a6;
+        publish(slots + (int64_t(k) * p.W + member) * kGenSlotWords + cc, val, tagA);
+      }
+    };
+
+    // Row merges of phase A for rows [k0, k1): wave wv takes rows k0 + wv,
+    // k0 + wv + kWaves, ...; lane j folds members j, j+64, ... in order, then
+    // a fixed DPP tree: every member obtains bit-identical row constants.
+    auto merge_a = [&](int k0, int k1) {
+      for (int k = k0 + wv; k < k1; k += kWaves) {
+        float a0[1] = {kNegInf}, a1[1] = {0.f}, a2[1] = {kNegInf}, a3[1] = {0.f};
+        float a4 = kNegInf, a5 = __builtin_bit_cast(float, INT_MAX), a6 = kNegInf;
+        for (int jm = lane; jm < p.W; jm += kWave) {
+          float q[kC];
+          collect<kC>(slots + (int64_t(k) * p.W + jm) * kGenSlotWords, tagA, p.err, q);
+          lse_fold(a0[0], a1[0], q[0], q[1]);
+          lse_fold(a2[0], a3[0], q[2], q[3]);
+          if constexpr (AM) argmax_fold(a4, a5, a6, q[4], q[kC - 2], q[kC - 1]);
+        }
+        wave_lse_n(a0, a1);
+        if constexpr (PQ) wave_lse_n(a2, a3);
+        if constexpr (AM) wave_argmax(a4, a5, a6);
+        if (lane == 0) {
+          const float mscd = a0[0], l2sd = __log2f(a1[0]);
+          const float msct = a2[0], l2st = PQ ? __log2f(a3[0]) : 0.f;
+          sh_row[k][0] = mscd;
+          sh_row[k][1] = l2sd;
+          sh_row[k][2] = msct;
+          sh_row[k][3] = l2st;
+          float aq = 0.f, px = 0.f;
+          int x = -1;
+          if (eal) {
+            float zdx, ztx;
+            if constexpr (AM) {
+              x = __builtin_bit_cast(int, a5);
+              zdx = a6;
+              ztx = a4;
+              if (x == INT_MAX) {  // no finite target logit: unspecified, stay in bounds
+                x = 0;
+                zdx = k < nvalid ? TI::load1(p.zd + (row0 + k) * int64_t(p.row_bytes), 0) : 0.f;
+                ztx = kNegInf;
+              }
+            } else {
+              x = k < nvalid ? sh_labx[parity][k] : 0;
+              zdx = k < nvalid ? sh_lab[parity][k][0] : 0.f;
+              ztx = k < nvalid ? sh_lab[parity][k][1] : kNegInf;
+            }
+            aq = ex2(__builtin_fmaf(zdx, p.scd, -mscd) - l2sd);
+            if constexpr (PQ) px = ex2(__builtin_fmaf(ztx, p.sct, -msct) - l2st);
+          }
+          sh_x[k] = x;
+          sh_row[k][4] = aq;
+          sh_row[k][5] = px;
+        }
+      }
+    };
+    // Phase B of rows [k0, k1): the present sums (TV: sum min(p, q) and Q<;
+    // KL), reduced over the workgroup and published.
+    auto phase_b = [&](auto k0c, auto k1c) {
+      constexpr int k0 = decltype(k0c)::value, k1 = decltype(k1c)::value, KG = k1 - k0;
+      pin_all();
+      float am[KG], aq[KG], ak[KG];
+#pragma unroll
+      for (int k = k0; k < k1; ++k) {
         const float mscd = sh_row[k][0];
         const float ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
         float sm = 0.f, sq = 0.f, sk = 0.f;
@@ -452,24 +467,23 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
             }
           }
         }
-        am[k] = sm;
-        aq[k] = sq;
-        ak[k] = sk;
+        am[k - k0] = sm;
+        aq[k - k0] = sq;
+        ak[k - k0] = sk;
       }
       {
-        // the present sums (TV: sum min and Q<; KL), reduced together
-        constexpr int C0 = TV ? 0 : 2;            // first component present
+        constexpr int C0 = TV ? 0 : 2;  // first component present
         constexpr int NC = (TV ? 2 : 0) + (KL ? 1 : 0);
-        constexpr int NB = NC * K;
+        constexpr int NB = NC * KG;
         constexpr int NP = (NB + 3) / 4 * 4;
         float vv[NP], vt[NP / 4];
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
+        for (int jr = 0; jr < KG; ++jr) {
           if constexpr (TV) {
-            vv[k] = am[k];
-            vv[K + k] = aq[k];
+            vv[jr] = am[jr];
+            vv[KG + jr] = aq[jr];
           }
-          if constexpr (KL) vv[(TV ? 2 * K : 0) + k] = ak[k];
+          if constexpr (KL) vv[(TV ? 2 * KG : 0) + jr] = ak[jr];
         }
 #pragma unroll
         for (int i = NB; i < NP; ++i) vv[i] = 0.f;
@@ -479,12 +493,12 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
 #pragma unroll
           for (int jq = 0; jq < NP / 4; ++jq) {
             const int i = 4 * jq + q;
-            if (i < NB) sh_w[wv][i % K][C0 + i / K] = vt[jq];
+            if (i < NB) sh_w[wv][k0 + i % KG][C0 + i / KG] = vt[jq];
           }
         }
         if (lane == 0) {
 #pragma unroll
-          for (int k = 0; k < K; ++k) {
+          for (int k = k0; k < k1; ++k) {
             if constexpr (!TV) {
               sh_w[wv][k][0] = 0.f;
               sh_w[wv][k][1] = 0.f;
@@ -494,8 +508,8 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         }
       }
       lds_barrier();
-      if (tid < 3 * K) {
-        const int k = tid / 3, cc = tid % 3;
+      if (tid < 3 * KG) {
+        const int k = k0 + tid / 3, cc = tid % 3;
         float r = sh_w[0][k][cc];
 #pragma unroll
         for (int i = 1; i < kWaves; ++i) r += sh_w[i][k][cc];
@@ -503,7 +517,10 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         if (cc == 2) r *= kLn2;
         publish(slots + (int64_t(k) * p.W + member) * kGenSlotWords + 8 + cc, r, tagB);
       }
-      for (int k = wv; k < K; k += kWaves) {
+    };
+    // Merges of phase B for rows [k0, k1), as for phase A.
+    auto merge_b = [&](int k0, int k1) {
+      for (int k = k0 + wv; k < k1; k += kWaves) {
         float r[3] = {0.f, 0.f, 0.f};
         for (int jm = lane; jm < p.W; jm += kWave) {
           float q[3];
@@ -519,10 +536,40 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           sh_b[k][2] = r[2];
         }
       }
-    } else if (tid < K) {
-      sh_b[tid][0] = 0.f;
-      sh_b[tid][1] = 0.f;
-      sh_b[tid][2] = 0.f;
+    };
+
+    // With a phase B the rows are split into two groups and the team merges
+    // pipelined: each group's partials are published as soon as they are
+    // complete and a merge is polled only after the other group's
+    // arithmetic, so three of the four merges of a chunk overlap arithmetic.
+    constexpr int K0 = PQ && K > 1 ? (K + 1) / 2 : K;
+    using I0 = std::integral_constant<int, 0>;
+    using IK0 = std::integral_constant<int, K0>;
+    using IK = std::integral_constant<int, K>;
+    phase_a(I0{}, IK0{});
+    if constexpr (K0 < K) phase_a(IK0{}, IK{});
+
+    // ------------------------------------------------------------ phase B
+    if constexpr (!PQ) {
+      merge_a(0, K);
+      if (tid < K) {
+        sh_b[tid][0] = 0.f;
+        sh_b[tid][1] = 0.f;
+        sh_b[tid][2] = 0.f;
+      }
+    } else if constexpr (K0 == K) {
+      merge_a(0, K);
+      lds_barrier();
+      phase_b(I0{}, IK{});
+      merge_b(0, K);
+    } else {
+      merge_a(0, K0);
+      lds_barrier();
+      phase_b(I0{}, IK0{});
+      merge_a(K0, K);
+      lds_barrier();
+      phase_b(IK0{}, IK{});
+      merge_b(0, K);
     }
     lds_barrier();
 
@@ -701,7 +748,12 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         }
       }
     }
-    lds_barrier();
+    // No barrier before the next chunk: a wave only reads and restages its
+    // own slice of the staging buffer (after its reads above have completed),
+    // the label data is double-buffered, and the shared row constants are
+    // rewritten only after the barrier closing the next chunk's first
+    // phase-A group, which every wave reaches after finishing this phase C.
+    wait_lds_all();
   }
   wait_vmem_all();
 }
