@@ -6,18 +6,25 @@
 // logit tensors into VGPRs (16-byte nontemporal loads) and keeps them there:
 //
 //   phase A  per-row max / sum-exp partials of the tempered draft and target
-//            (EAL: greedy-token partial instead of the target sum);
-//            published to the team through the workspace, team barrier 1.
-//   phase B  every member merges the W partials in member order (so every
-//            member holds bit-identical row normalisers).
-//            WTV: per-row partial sums of min(p, q) and Q< = sum_{q<p} q,
-//            published, team barrier 2, merged in member order.
-//            EAL: a = q(x*) from the one logit z_draft[x*] re-read from HBM.
+//            (EAL: the target's greedy token, with the draft logit there as
+//            a payload, instead of the target sum); published to the team.
+//   merge A  every member merges the W partials in member order (so every
+//            member holds bit-identical row normalisers; EAL's a = q(x*)
+//            follows from the payload).
+//   phase B  (WTV) per-row partial sums of min(p, q) and Q< = sum_{q<p} q,
+//            published, merged in member order.
 //   scan     prefix products / suffix sums over the K rows give E and the
 //            gradient coefficients (Eqs. eal_generic, loss_eal, loss_tv).
 //   phase C  gradient from the registers, 16-byte nontemporal stores; each
 //            register slot is refilled with the team's next window as soon
-//            as its gradient is written, so loads overlap the stores.
+//            as its gradient is written.
+//
+// WTV splits the rows into two groups and publishes each group's partials as
+// soon as they are complete, so that a merge is polled only after the other
+// group's arithmetic: of the four merges of a window only the last one waits.
+// The first pairs of the next window are staged into LDS during phase A and
+// copied to the registers in phase C; each wave stages and reads back only
+// its own threads' slots, so no barrier separates consecutive windows.
 //
 // The grid is persistent and launched cooperatively, so every member of a
 // team is resident.  Partials travel as 64-bit words {value, tag}: a reader

@@ -30,6 +30,11 @@
 //            the entry at x* is rewritten with its cX term by the thread
 //            that stored it.
 //
+// Variants with a phase B split the chunk's rows into two groups whose merges
+// overlap the other group's arithmetic, as in the EAL/WTV kernel, and no
+// barrier separates consecutive chunks (the staging buffer is per wave and
+// the label data is double-buffered by chunk parity).
+//
 // Rows of a chunk past the end of its sequence (when K does not divide S)
 // load as zeros and store nothing.  Polls are bounded; a timeout sets the
 // error word and the loss becomes NaN.
