@@ -163,6 +163,9 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     }
     __syncthreads();  // staging is read before the loop restages it
   }
+  // read once: a global load inside the scan would sit on every window's
+  // critical path
+  const double gscale = p.grad_scale ? double(*p.grad_scale) : 1.0;
   uint32_t iter = 0;
   for (; w < p.N; w += p.T, ++iter) {
     const int parity = iter & 1;
@@ -520,7 +523,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         pr *= double(a[k]);
         Ew += pr;
       }
-      const double scale = p.grad_scale ? double(*p.grad_scale) : 1.0;
+      const double scale = gscale;
       const double inv_n = 1.0 / double(p.N);
       double S = 1.0;
 #pragma unroll

@@ -64,6 +64,7 @@ struct GenResParams {
   int S;                  // positions per sequence (windows layout: K)
   int CS;                 // chunks per sequence
   int64_t Wn;             // windows
+  double inv_wn, inv_r;   // 1 / Wn (0 without windows), 1 / R
   int64_t R;              // rows
   int V, ng, W, T;
   uint32_t row_bytes, grow_bytes;
@@ -186,6 +187,10 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
     }
     __syncthreads();
   }
+  // read once: a global load inside the scan would sit on every chunk's
+  // critical path
+  const double gscale = p.grad_scale ? double(*p.grad_scale) : 1.0;
+  const double inv_k = 1.0 / double(K);
   uint32_t iter = 0;
   for (; c < p.NC; c += p.T, ++iter) {
     const int parity = iter & 1;
@@ -661,13 +666,11 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       }
       const int lo = max(0, s - K + 1), hi = min(s, p.S - K);
       const double count = hi >= lo ? double(hi - lo + 1) : 0.0;
-      const double scale = p.grad_scale ? double(*p.grad_scale) : 1.0;
-      const double f = scale * double(p.inv_t_d);
+      const double f = gscale * double(p.inv_t_d);
       const double a_tv = double(sh_b[k][0]), qlt = double(sh_b[k][1]), a_eal = double(sh_row[k][4]);
-      const double Wn = double(p.Wn);
-      const double g_tv = p.Wn > 0 ? (-double(p.w_wtv) * dtv - double(p.w_tv) * count / K) / Wn : 0.0;
-      const double g_eal = p.Wn > 0 ? -double(p.w_eal) * deal / Wn : 0.0;
-      const double g_kl = double(p.w_kl) / double(p.R);
+      const double g_tv = (-double(p.w_wtv) * dtv - double(p.w_tv) * count * inv_k) * p.inv_wn;
+      const double g_eal = -double(p.w_eal) * deal * p.inv_wn;
+      const double g_kl = double(p.w_kl) * p.inv_r;
       const double c_tv = g_tv * f, c_eal = g_eal * a_eal * f, c_kl = g_kl * f;
       const float cA = float(c_tv * (1.0 - qlt) - c_eal + c_kl);
       const float cB = float(-c_tv * qlt - c_eal + c_kl);
@@ -813,6 +816,8 @@ hipError_t launch_kg(const GenArgs& a, bool* used) {
   p.CS = CS;
   p.Wn = a.W;
   p.R = a.R;
+  p.inv_wn = a.W > 0 ? 1.0 / double(a.W) : 0.0;
+  p.inv_r = 1.0 / double(a.R);
   p.V = a.V;
   p.ng = ng;
   p.W = W;
