@@ -508,42 +508,49 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     }
 
     // --------------------------------------------------------------- scan
-    if (tid == 0) {
-      float a[K], qlt[K];
+    // Lane k of wave 0 evaluates row k's coefficient: every lane reads the
+    // K acceptances and forms P_k = prod_{j<k} a_j and S_k = 1 + a_{k+1} S_{k+1}
+    // in the order of the serial recurrences, so the results equal the
+    // one-thread form; lane 0 also sums E.
+    if (wv == 0) {
+      float a[K];
 #pragma unroll
-      for (int k = 0; k < K; ++k) {
-        a[k] = kWtv ? sh_coef[k][0] : sh_row[k][2];
-        qlt[k] = kWtv ? sh_coef[k][1] : 0.f;
-      }
-      double Pp[K];
-      double pr = 1.0, Ew = 0.0;
+      for (int j = 0; j < K; ++j) a[j] = kWtv ? sh_coef[j][0] : sh_row[j][2];
+      const int k = lane;
+      const bool own = k < K;
+      const float ak = own ? (kWtv ? sh_coef[k][0] : sh_row[k][2]) : 0.f;
+      const float qlt = (kWtv && own) ? sh_coef[k][1] : 0.f;
+      double P = 1.0, S = 1.0;
 #pragma unroll
-      for (int k = 0; k < K; ++k) {
-        Pp[k] = pr;
-        pr *= double(a[k]);
-        Ew += pr;
-      }
-      const double scale = gscale;
+      for (int j = 0; j < K; ++j)
+        if (j < k) P *= double(a[j]);
+#pragma unroll
+      for (int j = K - 1; j > 0; --j)
+        if (j > k) S = 1.0 + double(a[j]) * S;
       const double inv_n = 1.0 / double(p.N);
-      double S = 1.0;
-#pragma unroll
-      for (int k = K - 1; k >= 0; --k) {
-        const double g = -Pp[k] * S * inv_n;
-        const double factor = kWtv ? double(p.inv_t_d) : double(a[k]) * double(p.inv_t_d);
-        const float c = float(g * scale * factor);
+      const double g = -P * S * inv_n;
+      const double factor = kWtv ? double(p.inv_t_d) : double(ak) * double(p.inv_t_d);
+      const float c = float(g * gscale * factor);
+      if (own) {
         if constexpr (kWtv) {
-          sh_coef[k][0] = c * (1.f - qlt[k]);
-          sh_coef[k][1] = -c * qlt[k];
+          sh_coef[k][0] = c * (1.f - qlt);
+          sh_coef[k][1] = -c * qlt;
         } else {
           sh_coef[k][0] = c;
         }
-        S = 1.0 + double(a[k]) * S;
       }
       if (member == 0) {
-        p.window_e[w] = float(Ew);
+        if (lane == 0) {
+          double pr = 1.0, Ew = 0.0;
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          if (p.accept) p.accept[w * K + k] = a[k];
+          for (int j = 0; j < K; ++j) {
+            pr *= double(a[j]);
+            Ew += pr;
+          }
+          p.window_e[w] = float(Ew);
+        }
+        if (own) {
+          if (p.accept) p.accept[w * K + k] = ak;
           if constexpr (!kWtv) {
             if (p.xstar) p.xstar[w * K + k] = sh_x[k];
           }
