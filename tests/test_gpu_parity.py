@@ -87,6 +87,20 @@ def test_wtv_parity_shapes(A, dev, V, K, N, dtype, gdtype, path):
     _check_wtv(A, zd, zt, 1.0, 1.0, gdtype, _flags(A, path))
 
 
+# Small vocabularies with many windows: one workgroup per team and two to four
+# windows per team, so the fused schedule runs several windows per team (the
+# alternating slot planes, the row-group merges and the windows that follow
+# each other without a barrier), checked element by element.
+MANY = [(BF16, BF16, 1024, 7, 700), (BF16, F32, 4096, 5, 600), (F32, F32, 2048, 16, 800)]
+
+
+@pytest.mark.parametrize("dtype,gdtype,V,K,N", MANY)
+def test_many_windows_per_team(A, dev, dtype, gdtype, V, K, N):
+    zd, zt = _inputs("c1" if dtype == F32 else "c2", (N, K, V), dtype, seed=N + K, dev=dev)
+    _check_eal(A, zd, zt, 1.0, gdtype, 0)
+    _check_wtv(A, zd, zt, 0.7, 0.7, gdtype, 0)
+
+
 @pytest.mark.parametrize("T", [0.05, 0.5, 0.7, 1.0, 2.0])
 @pytest.mark.parametrize("dtype", [F32, BF16])
 def test_temperatures(A, dev, T, dtype):
