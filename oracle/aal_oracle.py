@@ -11,7 +11,7 @@ fp32 inputs are exactly representable in float64).  Array layout follows the
 library's: logits are ``[N, K, V]`` (N windows, K = the speculative window size
 gamma, V = vocabulary), row ``n*K + k`` is position ``k`` of window ``n``.
 
-Readings of places where the paper is silent (each is listed in the design doc):
+Readings of places where the paper is silent:
 
 * temperature: Eq. (1) scales log-probabilities; ``tempered_log_softmax``
   applies it literally to ``log softmax(z)``;
