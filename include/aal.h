@@ -298,6 +298,121 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
                               const float* grad_scale, void* workspace, size_t workspace_bytes,
                               void* stream);
 
+/*
+ * Vocabulary-parallel pieces of aal_eal_fwd_bwd and aal_wtv_fwd_bwd: the work
+ * of one rank of a tensor-parallel LM head that splits the vocabulary into
+ * contiguous slices.  The losses and gradients are those of the two calls
+ * above (Eq. acc_greedy, Eq. acc_sample, Eq. eal_generic, Eq. loss_eal,
+ * Eq. loss_tv); a row's softmax, greedy token and sum_v min(p, q) span all
+ * slices, so they are assembled from per-slice partial records that the
+ * caller gathers over the ranks (an all-gather of a few bytes per row) and
+ * every rank merges in the same rank order.  With R ranks, rank r holding
+ * vocabulary entries [v0_r, v0_r + Vs_r) of every row as its own contiguous
+ * [rows, Vs_r] arrays (rows = N*K, row stride Vs_r):
+ *
+ *   1. aal_vp_row_partials(slice)            -> part_r[rows]
+ *      gather part_r over r                  -> part_all[R][rows]   (caller)
+ *   2. aal_vp_merge_rows(part_all)           -> row[rows]           (same on every rank)
+ *   3. WTV only: aal_vp_accept_partials(slice, row) -> acc_r[rows]
+ *      gather acc_r over r                   -> acc_all[R][rows]    (caller)
+ *   4. aal_vp_window_scan(row, acc_all)      -> loss, E_n, a, x*, row[].coef
+ *   5. aal_vp_grad(slice, row)               -> grad_draft slice [rows, Vs_r]
+ *
+ * Records are plain structs so that a collective can move them as bytes.
+ * Every value is a function of the inputs and R's slicing alone: each rank
+ * obtains bit-identical row records, and the results do not depend on which
+ * rank runs steps 2 and 4.  Conventions (device pointers, streams, 16-byte
+ * alignment of logit and gradient pointers, errors) are those stated at the
+ * top of this file; these calls take no workspace.  Temperatures must be the
+ * same in every call of one pass.
+ */
+typedef enum { AAL_VP_EAL = 0, AAL_VP_WTV = 1 } aal_vp_mode_t;
+
+/* Partial statistics of one row over one vocabulary slice.  32 bytes.
+ *   zmax_d, zmax_t : largest raw draft / target logit in the slice (-inf if none)
+ *   s_d, s_t       : sum over the slice of 2^(z*sc - fl(zmax*sc)), sc = log2(e)/T
+ *                    (s_t is 0 in EAL mode)
+ *   zd_at          : EAL: the draft logit at t_idx (0 if t_idx is INT32_MAX)
+ *   t_idx          : EAL: global index of the slice's largest target logit,
+ *                    lowest index on ties, INT32_MAX if the slice has no finite
+ *                    target logit; WTV: -1 */
+typedef struct {
+  float zmax_d, s_d, zmax_t, s_t, zd_at;
+  int32_t t_idx, reserved0, reserved1;
+} aal_vp_part_t;
+
+/* Partial sums of one row over one slice (WTV): sum_v min(p, q) and
+ * Q< = sum over entries with q < p of q, with the merged normalisers. */
+typedef struct {
+  float smin, qlt;
+} aal_vp_acc_t;
+
+/* Merged record of one row.  32 bytes.
+ *   msc_d, msc_t : fl(zmax * sc) of the whole row, the reference of l2s_*
+ *   l2s_d, l2s_t : log2 of sum_v 2^(z*sc - msc), so log2 q(v) = z*sc - msc_d - l2s_d
+ *                  (msc_t, l2s_t are 0 in EAL mode)
+ *   a            : acceptance (EAL: q(x*), set by step 2; WTV: sum min(p, q), step 4)
+ *   qlt          : WTV: Q< (step 4); EAL: 0
+ *   coef         : gradient coefficient of the row (step 4)
+ *   xstar        : EAL: greedy target token (0 for a row with no finite target
+ *                  logit); WTV: -1 */
+typedef struct {
+  float msc_d, l2s_d, msc_t, l2s_t, a, qlt, coef;
+  int32_t xstar;
+} aal_vp_row_t;
+
+/*
+ * Step 1.  z_draft, z_target : [rows, V_slice] of in_dtype, the slice that
+ * starts at global vocabulary index v0.  rows >= 1, V_slice >= 1, v0 >= 0,
+ * v0 + V_slice < 2^31, rows*V_slice < 2^62.  EAL ignores temp_target.
+ * parts : [rows] records, required.
+ */
+aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
+                                 int64_t rows, int32_t V_slice, int32_t v0, aal_vp_mode_t mode,
+                                 float temp_draft, float temp_target, aal_vp_part_t* parts,
+                                 void* stream);
+
+/*
+ * Step 2.  parts_all : [R, rows] records, rank-major (rank r's records at
+ * parts_all + r*rows), R >= 1.  Merged in rank order 0..R-1: the maxima, the
+ * sums rescaled to them, the greedy token by (largest logit, lowest index).
+ * Every row needs a finite draft logit (and in WTV a finite target logit) in
+ * some slice.  row : [rows] records, required; EAL sets a and xstar.
+ */
+aal_status_t aal_vp_merge_rows(const aal_vp_part_t* parts_all, int32_t R, int64_t rows,
+                               aal_vp_mode_t mode, float temp_draft, float temp_target,
+                               aal_vp_row_t* row, void* stream);
+
+/*
+ * Step 3 (WTV).  The slice as in step 1, row from step 2.  acc : [rows], required.
+ */
+aal_status_t aal_vp_accept_partials(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
+                                    int64_t rows, int32_t V_slice, float temp_draft, float temp_target,
+                                    const aal_vp_row_t* row, aal_vp_acc_t* acc, void* stream);
+
+/*
+ * Step 4.  row : [N*K] records from step 2, updated in place (WTV: a and qlt
+ * summed from acc_all in rank order; both modes: coef).  acc_all : [R, N*K],
+ * rank-major, required for WTV and ignored (may be NULL) for EAL.
+ * N >= 1, 1 <= K <= 64, N*K < 2^31.  loss [1] and eal_per_window [N] are
+ * required; accept [N*K] and target_argmax [N*K] (EAL) may be NULL.  grad_scale
+ * as for aal_eal_fwd_bwd.
+ */
+aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R,
+                                int64_t N, int32_t K, aal_vp_mode_t mode, float temp_draft,
+                                const float* grad_scale, float* loss, float* eal_per_window,
+                                float* accept, int32_t* target_argmax, void* stream);
+
+/*
+ * Step 5.  The slice as in step 1 (EAL reads only z_draft; z_target may then be
+ * NULL), row from step 4.  grad_draft : [rows, V_slice] of grad_dtype, the
+ * slice of the gradient of the loss, times *grad_scale as folded into coef.
+ */
+aal_status_t aal_vp_grad(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
+                         int64_t rows, int32_t V_slice, int32_t v0, aal_vp_mode_t mode,
+                         float temp_draft, float temp_target, const aal_vp_row_t* row,
+                         void* grad_draft, aal_dtype_t grad_dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -10,12 +10,19 @@ from .api import (  # noqa: F401
     AAL_FLAG_STREAMING,
     AAL_LAYOUT_SEQUENCES,
     AAL_LAYOUT_WINDOWS,
+    AAL_VP_EAL,
+    AAL_VP_WTV,
     aal_eal_fwd_bwd,
     aal_grpo_fwd_bwd,
     aal_grpo_workspace_bytes,
     aal_loss_fwd_bwd,
     aal_loss_workspace_bytes,
     aal_sim_accept_grpo,
+    aal_vp_accept_partials,
+    aal_vp_grad,
+    aal_vp_merge_rows,
+    aal_vp_row_partials,
+    aal_vp_window_scan,
     aal_workspace_bytes,
     aal_wtv_fwd_bwd,
     workspace,

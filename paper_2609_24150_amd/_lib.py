@@ -21,6 +21,12 @@ AAL_ERR_HIP = 5
 AAL_FLAG_STREAMING = 1
 AAL_LAYOUT_WINDOWS = 0
 AAL_LAYOUT_SEQUENCES = 1
+AAL_VP_EAL = 0
+AAL_VP_WTV = 1
+# Record sizes of aal_vp_part_t, aal_vp_acc_t and aal_vp_row_t (bytes).
+VP_PART_BYTES = 32
+VP_ACC_BYTES = 8
+VP_ROW_BYTES = 32
 
 
 class LossWeights(C.Structure):
@@ -65,6 +71,16 @@ _SIGNATURES = {
         _vp, _vp, _vp, _vp, C.c_int, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
         C.c_int32, _vp, C.c_float, GrpoParams, _vp, _vp, _vp, _vp, _vp,
         _vp, C.c_int, _vp, _vp, C.c_size_t, _vp]),
+    "aal_vp_row_partials": (C.c_int, [
+        _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_float, C.c_float, _vp, _vp]),
+    "aal_vp_merge_rows": (C.c_int, [_vp, C.c_int32, C.c_int64, C.c_int, C.c_float, C.c_float, _vp, _vp]),
+    "aal_vp_accept_partials": (C.c_int, [
+        _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_float, C.c_float, _vp, _vp, _vp]),
+    "aal_vp_window_scan": (C.c_int, [
+        _vp, _vp, C.c_int32, C.c_int64, C.c_int32, C.c_int, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "aal_vp_grad": (C.c_int, [
+        _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_float, C.c_float, _vp, _vp, C.c_int,
+        _vp]),
 }
 
 _lib = None

@@ -8,7 +8,9 @@ from __future__ import annotations
 import torch
 
 from . import _lib
-from ._lib import AAL_BF16, AAL_F32, AAL_FLAG_STREAMING, AAL_LAYOUT_SEQUENCES, AAL_LAYOUT_WINDOWS  # noqa: F401
+from ._lib import (  # noqa: F401
+    AAL_BF16, AAL_F32, AAL_FLAG_STREAMING, AAL_LAYOUT_SEQUENCES, AAL_LAYOUT_WINDOWS, AAL_VP_EAL, AAL_VP_WTV,
+)
 
 _DT = {torch.bfloat16: AAL_BF16, torch.float32: AAL_F32}
 
@@ -263,3 +265,112 @@ def aal_grpo_fwd_bwd(z_theta: torch.Tensor, z_ref: torch.Tensor, z_target: torch
         _ptr(ws), ws.numel(), _stream(dev, stream))
     _lib.check(st, "aal_grpo_fwd_bwd")
     return out
+
+
+# ----------------------------------------------------------------------------
+# Vocabulary-parallel pieces (one rank's share of a vocabulary-split LM head).
+# Records are uint8 device tensors of shape [rows, record bytes]; view them as
+# float32 / int32 to read fields.  The caller gathers the records over ranks.
+
+def _vp_slice(z_draft, z_target, need_target=True):
+    if z_draft.dim() != 2:
+        raise ValueError("vocabulary slices are [rows, V_slice]")
+    if need_target or z_target is not None:
+        _check_logits(z_draft, z_target, 2)
+    elif not (z_draft.is_cuda and z_draft.is_contiguous()):
+        raise ValueError("z_draft must be a contiguous device tensor")
+    return z_draft.shape[0], z_draft.shape[1], z_draft.device
+
+
+def _records(t: torch.Tensor, nbytes: int, name: str, lead: int):
+    if t.dtype != torch.uint8 or t.dim() != lead + 1 or t.shape[-1] != nbytes or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous uint8 tensor of records of {nbytes} bytes")
+
+
+def aal_vp_row_partials(z_draft: torch.Tensor, z_target: torch.Tensor, v0: int, mode: int,
+                        temp_draft: float = 1.0, temp_target: float = 1.0, *, stream=None) -> torch.Tensor:
+    """Step 1: partial row statistics of the slice [v0, v0 + V_slice).  Returns [rows, 32] records."""
+    rows, vs, dev = _vp_slice(z_draft, z_target)
+    parts = torch.empty(rows, _lib.VP_PART_BYTES, dtype=torch.uint8, device=dev)
+    st = _lib.lib().aal_vp_row_partials(_ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), rows, vs, int(v0),
+                                        int(mode), float(temp_draft), float(temp_target), _ptr(parts),
+                                        _stream(dev, stream))
+    _lib.check(st, "aal_vp_row_partials")
+    return parts
+
+
+def aal_vp_merge_rows(parts_all: torch.Tensor, mode: int, temp_draft: float = 1.0, temp_target: float = 1.0, *,
+                      stream=None) -> torch.Tensor:
+    """Step 2: merge gathered partials [R, rows, 32] in rank order.  Returns [rows, 32] row records."""
+    _records(parts_all, _lib.VP_PART_BYTES, "parts_all", 2)
+    R, rows = parts_all.shape[0], parts_all.shape[1]
+    dev = parts_all.device
+    row = torch.empty(rows, _lib.VP_ROW_BYTES, dtype=torch.uint8, device=dev)
+    st = _lib.lib().aal_vp_merge_rows(_ptr(parts_all), R, rows, int(mode), float(temp_draft), float(temp_target),
+                                      _ptr(row), _stream(dev, stream))
+    _lib.check(st, "aal_vp_merge_rows")
+    return row
+
+
+def aal_vp_accept_partials(z_draft: torch.Tensor, z_target: torch.Tensor, row: torch.Tensor,
+                           temp_draft: float = 1.0, temp_target: float = 1.0, *, stream=None) -> torch.Tensor:
+    """Step 3 (WTV): the slice's sum min(p, q) and Q< partials.  Returns [rows, 8] records."""
+    rows, vs, dev = _vp_slice(z_draft, z_target)
+    _records(row, _lib.VP_ROW_BYTES, "row", 1)
+    if row.shape[0] != rows:
+        raise ValueError("row must hold one record per logit row")
+    acc = torch.empty(rows, _lib.VP_ACC_BYTES, dtype=torch.uint8, device=dev)
+    st = _lib.lib().aal_vp_accept_partials(_ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), rows, vs,
+                                           float(temp_draft), float(temp_target), _ptr(row), _ptr(acc),
+                                           _stream(dev, stream))
+    _lib.check(st, "aal_vp_accept_partials")
+    return acc
+
+
+def aal_vp_window_scan(row: torch.Tensor, acc_all: torch.Tensor | None, N: int, K: int, mode: int,
+                       temp_draft: float = 1.0, *, grad_scale: torch.Tensor | None = None, stream=None) -> dict:
+    """Step 4: window scan over the merged rows (updated in place with a, qlt
+    and coef).  acc_all [R, N*K, 8] in WTV mode.  Returns loss [1], E [N],
+    accept [N, K] and, in EAL mode, xstar [N, K]."""
+    _records(row, _lib.VP_ROW_BYTES, "row", 1)
+    if row.shape[0] != N * K:
+        raise ValueError("row must hold N*K records")
+    dev = row.device
+    R = 0
+    if mode == _lib.AAL_VP_WTV:
+        if acc_all is None:
+            raise ValueError("acc_all is required in WTV mode")
+        _records(acc_all, _lib.VP_ACC_BYTES, "acc_all", 2)
+        if acc_all.shape[1] != N * K:
+            raise ValueError("acc_all must be [R, N*K, 8]")
+        R = acc_all.shape[0]
+    if grad_scale is not None and (grad_scale.dtype != torch.float32 or grad_scale.device != dev):
+        raise TypeError("grad_scale must be a float32 device tensor")
+    out = {
+        "loss": torch.empty(1, dtype=torch.float32, device=dev),
+        "E": torch.empty(N, dtype=torch.float32, device=dev),
+        "accept": torch.empty(N, K, dtype=torch.float32, device=dev),
+    }
+    if mode == _lib.AAL_VP_EAL:
+        out["xstar"] = torch.empty(N, K, dtype=torch.int32, device=dev)
+    st = _lib.lib().aal_vp_window_scan(_ptr(row), _ptr(acc_all) if R else None, R, N, K, int(mode),
+                                       float(temp_draft), _ptr(grad_scale), _ptr(out["loss"]), _ptr(out["E"]),
+                                       _ptr(out["accept"]), _ptr(out.get("xstar")), _stream(dev, stream))
+    _lib.check(st, "aal_vp_window_scan")
+    return out
+
+
+def aal_vp_grad(z_draft: torch.Tensor, z_target: torch.Tensor | None, row: torch.Tensor, v0: int, mode: int,
+                temp_draft: float = 1.0, temp_target: float = 1.0, *, grad_dtype: torch.dtype | None = None,
+                stream=None) -> torch.Tensor:
+    """Step 5: the slice [v0, v0 + V_slice) of dloss/dz_draft.  Returns [rows, V_slice]."""
+    rows, vs, dev = _vp_slice(z_draft, z_target, need_target=(mode == _lib.AAL_VP_WTV))
+    _records(row, _lib.VP_ROW_BYTES, "row", 1)
+    if row.shape[0] != rows:
+        raise ValueError("row must hold one record per logit row")
+    g = torch.empty(rows, vs, dtype=grad_dtype or z_draft.dtype, device=dev)
+    st = _lib.lib().aal_vp_grad(_ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), rows, vs, int(v0),
+                                int(mode), float(temp_draft), float(temp_target), _ptr(row), _ptr(g),
+                                _dtype_code(g.dtype), _stream(dev, stream))
+    _lib.check(st, "aal_vp_grad")
+    return g

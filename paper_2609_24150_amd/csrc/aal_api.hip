@@ -2,6 +2,7 @@
 // Declarations and the contract of every entry point are in include/aal.h.
 #include "aal.h"
 #include "aal_internal.h"
+#include "aal_vp.h"
 
 #include <stdarg.h>
 #include <stdio.h>
@@ -91,6 +92,37 @@ aal_status_t run_loss(aal::LossArgs& a, uint32_t flags) {
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
 }
+
+// Shared checks of the vocabulary-parallel slice calls.
+aal_status_t validate_vp_slice(const void* zd, const void* zt, bool need_zt, int in_dtype, int64_t rows,
+                               int32_t vs, int32_t v0) {
+  if (!zd || (need_zt && !zt)) return fail(AAL_ERR_ARG, "z_draft and z_target must be non-NULL");
+  if (rows < 1) return fail(AAL_ERR_ARG, "rows must be >= 1 (got %lld)", (long long)rows);
+  if (vs < 1) return fail(AAL_ERR_ARG, "V_slice must be >= 1 (got %d)", vs);
+  if (v0 < 0 || int64_t(v0) + vs > int64_t(INT32_MAX))
+    return fail(AAL_ERR_ARG, "v0 must be >= 0 with v0 + V_slice < 2^31 (got v0 = %d)", v0);
+  if (rows > (int64_t(1) << 62) / vs) return fail(AAL_ERR_ARG, "rows*V_slice must be < 2^62");
+  if (!valid_dtype(in_dtype)) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", in_dtype);
+  if (!aligned(zd, 16) || (zt && !aligned(zt, 16))) return fail(AAL_ERR_ALIGN, "logit pointers must be 16-byte aligned");
+  return AAL_OK;
+}
+
+bool valid_vp_mode(int m) { return m == AAL_VP_EAL || m == AAL_VP_WTV; }
+
+aal_status_t vp_scales(int mode, float temp_draft, float temp_target, float* scd, float* sct) {
+  *scd = scale_for(temp_draft);
+  if (!positive_finite(temp_draft) || *scd == 0.f)
+    return fail(AAL_ERR_ARG, "temp_draft must be finite, > 0 and >= 1e-37");
+  *sct = 0.f;
+  if (mode == AAL_VP_WTV) {
+    *sct = scale_for(temp_target);
+    if (!positive_finite(temp_target) || *sct == 0.f)
+      return fail(AAL_ERR_ARG, "temp_target must be finite, > 0 and >= 1e-37");
+  }
+  return AAL_OK;
+}
+
+aal::Mode vp_mode(int m) { return m == AAL_VP_EAL ? aal::Mode::kEal : aal::Mode::kWtv; }
 
 }  // namespace
 
@@ -457,6 +489,123 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
   a.group_loss = reinterpret_cast<float*>(wp);
   a.stream = static_cast<hipStream_t>(stream);
   hipError_t e = aal::launch_grpo(a);
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
+
+aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t rows,
+                                 int32_t V_slice, int32_t v0, aal_vp_mode_t mode, float temp_draft,
+                                 float temp_target, aal_vp_part_t* parts, void* stream) {
+  g_last_error.clear();
+  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
+  aal_status_t st = validate_vp_slice(z_draft, z_target, true, int(in_dtype), rows, V_slice, v0);
+  if (st != AAL_OK) return st;
+  if (!parts) return fail(AAL_ERR_ARG, "parts must be non-NULL");
+  if (!aligned(parts, 4)) return fail(AAL_ERR_ALIGN, "parts must be 4-byte aligned");
+  aal::VpSlice s{};
+  if ((st = vp_scales(int(mode), temp_draft, temp_target, &s.scd, &s.sct)) != AAL_OK) return st;
+  s.zd = z_draft;
+  s.zt = z_target;
+  s.in = to_dtype(in_dtype);
+  s.rows = rows;
+  s.vs = V_slice;
+  s.v0 = v0;
+  s.mode = vp_mode(int(mode));
+  s.stream = static_cast<hipStream_t>(stream);
+  const hipError_t e = aal::launch_vp_partials(s, parts);
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
+aal_status_t aal_vp_merge_rows(const aal_vp_part_t* parts_all, int32_t R, int64_t rows, aal_vp_mode_t mode,
+                               float temp_draft, float temp_target, aal_vp_row_t* row, void* stream) {
+  g_last_error.clear();
+  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
+  if (!parts_all || !row) return fail(AAL_ERR_ARG, "parts_all and row must be non-NULL");
+  if (R < 1) return fail(AAL_ERR_ARG, "R must be >= 1 (got %d)", R);
+  if (rows < 1) return fail(AAL_ERR_ARG, "rows must be >= 1 (got %lld)", (long long)rows);
+  if (rows > (int64_t(1) << 56) / R) return fail(AAL_ERR_ARG, "R*rows must be < 2^56");
+  if (!aligned(parts_all, 4) || !aligned(row, 4)) return fail(AAL_ERR_ALIGN, "records must be 4-byte aligned");
+  float scd, sct;
+  aal_status_t st = vp_scales(int(mode), temp_draft, temp_target, &scd, &sct);
+  if (st != AAL_OK) return st;
+  const hipError_t e =
+      aal::launch_vp_merge(parts_all, R, rows, vp_mode(int(mode)), scd, sct, row, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
+aal_status_t aal_vp_accept_partials(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t rows,
+                                    int32_t V_slice, float temp_draft, float temp_target, const aal_vp_row_t* row,
+                                    aal_vp_acc_t* acc, void* stream) {
+  g_last_error.clear();
+  aal_status_t st = validate_vp_slice(z_draft, z_target, true, int(in_dtype), rows, V_slice, 0);
+  if (st != AAL_OK) return st;
+  if (!row || !acc) return fail(AAL_ERR_ARG, "row and acc must be non-NULL");
+  if (!aligned(row, 4) || !aligned(acc, 4)) return fail(AAL_ERR_ALIGN, "records must be 4-byte aligned");
+  aal::VpSlice s{};
+  if ((st = vp_scales(AAL_VP_WTV, temp_draft, temp_target, &s.scd, &s.sct)) != AAL_OK) return st;
+  s.zd = z_draft;
+  s.zt = z_target;
+  s.in = to_dtype(in_dtype);
+  s.rows = rows;
+  s.vs = V_slice;
+  s.v0 = 0;
+  s.mode = aal::Mode::kWtv;
+  s.stream = static_cast<hipStream_t>(stream);
+  const hipError_t e = aal::launch_vp_accept(s, row, acc);
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
+aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R, int64_t N, int32_t K,
+                                aal_vp_mode_t mode, float temp_draft, const float* grad_scale, float* loss,
+                                float* eal_per_window, float* accept, int32_t* target_argmax, void* stream) {
+  g_last_error.clear();
+  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
+  if (!row || !loss || !eal_per_window) return fail(AAL_ERR_ARG, "row, loss and eal_per_window must be non-NULL");
+  if (N < 1) return fail(AAL_ERR_ARG, "N must be >= 1 (got %lld)", (long long)N);
+  if (K < 1 || K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", K);
+  if (N > (int64_t(1) << 31) / K) return fail(AAL_ERR_ARG, "N*K must be < 2^31");
+  const bool wtv = mode == AAL_VP_WTV;
+  if (wtv && !acc_all) return fail(AAL_ERR_ARG, "acc_all must be non-NULL in WTV mode");
+  if (wtv && R < 1) return fail(AAL_ERR_ARG, "R must be >= 1 (got %d)", R);
+  if (wtv && N * K > (int64_t(1) << 56) / R) return fail(AAL_ERR_ARG, "R*N*K must be < 2^56");
+  if (!aligned(row, 4) || (wtv && !aligned(acc_all, 4))) return fail(AAL_ERR_ALIGN, "records must be 4-byte aligned");
+  float scd, sct;
+  aal_status_t st = vp_scales(AAL_VP_EAL, temp_draft, 1.f, &scd, &sct);
+  if (st != AAL_OK) return st;
+  const hipError_t e = aal::launch_vp_scan(row, wtv ? acc_all : nullptr, wtv ? R : 0, N, K, vp_mode(int(mode)),
+                                           1.0f / temp_draft, grad_scale, loss, eal_per_window, accept,
+                                           wtv ? nullptr : target_argmax, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
+aal_status_t aal_vp_grad(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t rows,
+                         int32_t V_slice, int32_t v0, aal_vp_mode_t mode, float temp_draft, float temp_target,
+                         const aal_vp_row_t* row, void* grad_draft, aal_dtype_t grad_dtype, void* stream) {
+  g_last_error.clear();
+  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
+  aal_status_t st =
+      validate_vp_slice(z_draft, z_target, mode == AAL_VP_WTV, int(in_dtype), rows, V_slice, v0);
+  if (st != AAL_OK) return st;
+  if (!row || !grad_draft) return fail(AAL_ERR_ARG, "row and grad_draft must be non-NULL");
+  if (!valid_dtype(int(grad_dtype))) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", int(grad_dtype));
+  if (!aligned(row, 4)) return fail(AAL_ERR_ALIGN, "records must be 4-byte aligned");
+  if (!aligned(grad_draft, 16)) return fail(AAL_ERR_ALIGN, "grad_draft must be 16-byte aligned");
+  aal::VpSlice s{};
+  if ((st = vp_scales(int(mode), temp_draft, temp_target, &s.scd, &s.sct)) != AAL_OK) return st;
+  s.zd = z_draft;
+  s.zt = mode == AAL_VP_WTV ? z_target : nullptr;
+  s.in = to_dtype(in_dtype);
+  s.rows = rows;
+  s.vs = V_slice;
+  s.v0 = v0;
+  s.mode = vp_mode(int(mode));
+  s.stream = static_cast<hipStream_t>(stream);
+  const hipError_t e = aal::launch_vp_grad(s, row, grad_draft, to_dtype(grad_dtype));
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
 }

@@ -160,3 +160,40 @@ def test_grpo_validation(lib, kw, code):
     L = lib.lib()
     assert _grpo(L, lib, **kw) == code
     assert L.aal_last_error().decode() != ""
+
+
+def test_vp_validation(lib):
+    """Every case fails validation, so no kernel is launched."""
+    L = lib.lib()
+    P = L.aal_vp_row_partials
+
+    def part(zd=16, zt=16, dt=0, rows=2, vs=8, v0=0, mode=0, td=1.0, tt=1.0, parts=16):
+        return P(zd, zt, dt, rows, vs, v0, mode, td, tt, parts, None)
+
+    for kw, code in [(dict(rows=0), 1), (dict(vs=0), 1), (dict(v0=-1), 1), (dict(v0=(1 << 31) - 4), 1),
+                     (dict(dt=5), 2), (dict(zd=18), 3), (dict(zt=None), 1), (dict(mode=9), 1),
+                     (dict(mode=1, tt=0.0), 1), (dict(td=float("nan")), 1), (dict(parts=None), 1),
+                     (dict(parts=18), 3), (dict(rows=1 << 60), 1)]:
+        assert part(**kw) == code, kw
+        assert L.aal_last_error().decode() != ""
+    M = L.aal_vp_merge_rows
+    assert M(16, 0, 4, 0, 1.0, 1.0, 16, None) == 1
+    assert M(16, 2, 0, 0, 1.0, 1.0, 16, None) == 1
+    assert M(None, 2, 4, 0, 1.0, 1.0, 16, None) == 1
+    assert M(16, 2, 4, 1, 1.0, -1.0, 16, None) == 1
+    assert M(16, 2, 4, 3, 1.0, 1.0, 16, None) == 1
+    Acc = L.aal_vp_accept_partials
+    assert Acc(16, 16, 0, 2, 8, 1.0, 1.0, None, 16, None) == 1
+    assert Acc(16, None, 0, 2, 8, 1.0, 1.0, 16, 16, None) == 1
+    S = L.aal_vp_window_scan
+    assert S(16, None, 1, 2, 3, 1, 1.0, None, 16, 16, None, None, None) == 1   # WTV needs acc_all
+    assert S(16, 16, 1, 2, 65, 0, 1.0, None, 16, 16, None, None, None) == 1
+    assert S(16, 16, 1, 0, 3, 0, 1.0, None, 16, 16, None, None, None) == 1
+    assert S(16, 16, 1, 2, 3, 0, 1.0, None, None, 16, None, None, None) == 1
+    assert S(16, 16, 1, 2, 3, 0, 1.0, None, 16, None, None, None, None) == 1
+    assert S(16, 16, 1, 2, 3, 0, 0.0, None, 16, 16, None, None, None) == 1
+    G = L.aal_vp_grad
+    assert G(16, 16, 0, 2, 8, 0, 1, 1.0, 1.0, 16, None, 0, None) == 1
+    assert G(16, 16, 0, 2, 8, 0, 1, 1.0, 1.0, 16, 16, 9, None) == 2
+    assert G(16, 16, 0, 2, 8, 0, 1, 1.0, 1.0, 16, 24, 0, None) == 3
+    assert G(16, None, 0, 2, 8, 0, 1, 1.0, 1.0, 16, 16, 0, None) == 1   # WTV reads the target
