@@ -217,6 +217,45 @@ def general_call(zd, zt, layout, B, S, K, weights, grad_dtype):
     return fn, stream, R, W
 
 
+def vp_call(zd_s, zt_s, v0, R, N, K, mode, grad_dtype):
+    """A zero-allocation closure over one rank's five vocabulary-parallel calls
+    on its [rows, V_slice] slice.  The rank's own records copied into every
+    rank's place stand in for the two all-gathers' outputs."""
+    import torch
+
+    from paper_2609_24150_amd import _lib
+    rows, vs = zd_s.shape
+    dev = zd_s.device
+    L = _lib.lib()
+    stream = torch.cuda.current_stream(dev)
+    parts = torch.empty(R, rows, _lib.VP_PART_BYTES, dtype=torch.uint8, device=dev)
+    row = torch.empty(rows, _lib.VP_ROW_BYTES, dtype=torch.uint8, device=dev)
+    acc = torch.empty(R, rows, _lib.VP_ACC_BYTES, dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, device=dev)
+    E = torch.empty(N, device=dev)
+    grad = torch.empty(rows, vs, dtype=grad_dtype, device=dev)
+    dcode = _lib.AAL_BF16 if zd_s.dtype == torch.bfloat16 else _lib.AAL_F32
+    gcode = _lib.AAL_BF16 if grad_dtype == torch.bfloat16 else _lib.AAL_F32
+    wtv = mode == _lib.AAL_VP_WTV
+    s = stream.cuda_stream
+
+    def fn():
+        _lib.check(L.aal_vp_row_partials(zd_s.data_ptr(), zt_s.data_ptr(), dcode, rows, vs, v0, mode, 1.0, 1.0,
+                                         parts[0].data_ptr(), s), "aal_vp_row_partials")
+        parts[1:].copy_(parts[0].expand(R - 1, -1, -1))
+        _lib.check(L.aal_vp_merge_rows(parts.data_ptr(), R, rows, mode, 1.0, 1.0, row.data_ptr(), s),
+                   "aal_vp_merge_rows")
+        if wtv:
+            _lib.check(L.aal_vp_accept_partials(zd_s.data_ptr(), zt_s.data_ptr(), dcode, rows, vs, 1.0, 1.0,
+                                                row.data_ptr(), acc[0].data_ptr(), s), "aal_vp_accept_partials")
+            acc[1:].copy_(acc[0].expand(R - 1, -1, -1))
+        _lib.check(L.aal_vp_window_scan(row.data_ptr(), acc.data_ptr() if wtv else None, R, N, K, mode, 1.0, None,
+                                        loss.data_ptr(), E.data_ptr(), None, None, s), "aal_vp_window_scan")
+        _lib.check(L.aal_vp_grad(zd_s.data_ptr(), zt_s.data_ptr() if wtv else None, dcode, rows, vs, v0, mode,
+                                 1.0, 1.0, row.data_ptr(), grad.data_ptr(), gcode, s), "aal_vp_grad")
+    return fn, stream
+
+
 def grpo_call(zth, zref, zt, m, K, grad_dtype):
     """A zero-allocation closure over aal_grpo_fwd_bwd (windows layout, groups of m windows)."""
     import torch
@@ -353,6 +392,19 @@ def main():
             also["grpo_c2_m8"] = {"ms": ms_r, "rows_per_s": rows / (ms_r * 1e-3), "windows_per_s": N / (ms_r * 1e-3),
                                   "alg_GBps": rows * (3 * s_in + s_g) * V / (ms_r * 1e-3) / 1e9,
                                   "entry": "aal_grpo_fwd_bwd", "groups": N // m_, "m": m_}
+            # one rank's share of the same rows with the vocabulary split over 8
+            # ranks (a vocabulary-parallel LM head): slice 3 of 8
+            R_vp = 8
+            vs = V // R_vp
+            zd_s = zd.view(rows, V)[:, 3 * vs:4 * vs].contiguous()
+            zt_s = zt.view(rows, V)[:, 3 * vs:4 * vs].contiguous()
+            for name, mode in (("vp_wtv_c2_rank_share_8", _lib.AAL_VP_WTV), ("vp_eal_c2_rank_share_8", _lib.AAL_VP_EAL)):
+                fn_v, st_v = vp_call(zd_s, zt_s, 3 * vs, R_vp, N, K, mode, gdt)
+                ms_v = _time_calls(fn_v, args.steps, args.warmup, st_v)
+                also[name] = {"ms": ms_v, "rows_per_s": rows / (ms_v * 1e-3),
+                              "alg_GBps": rows * (2 * s_in + s_g) * vs / (ms_v * 1e-3) / 1e9,
+                              "entry": "aal_vp_*", "shape": f"{rows}x{vs} (V={V} over {R_vp} ranks)"}
+            del zd_s, zt_s
             del zd, zt, zref
         del inp
         torch.cuda.empty_cache()
