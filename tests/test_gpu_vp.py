@@ -171,3 +171,44 @@ def test_vp_argument_errors(A, dev):
         A.aal_vp_row_partials(d, t, 0, 7)
     with pytest.raises(A.AalError):
         A.aal_vp_row_partials(d, t, 0, A.AAL_VP_WTV, 1.0, 0.0)
+
+
+@pytest.mark.parametrize("mode", ["wtv", "eal"])
+def test_vp_full_c2_over_8_ranks(A, dev, mode):
+    """The c2 workload (2048 windows x 7 x 128256, bf16) with the vocabulary over
+    8 ranks of 16032 entries, every slice at full size; the oracle recomputes a
+    sample of windows, and over all windows the loss equals -mean(E)."""
+    import gc
+
+    from paper_2609_24150_amd.inputs import make_config
+    inp = make_config("c2", seed=0, device=dev)
+    zd, zt = inp["z_draft"], inp["z_target"]
+    N, K, V = zd.shape
+    m = A.AAL_VP_WTV if mode == "wtv" else A.AAL_VP_EAL
+    r = run_vp(A, zd, zt, m, [V // 8] * 8)
+    E = host64(r["E"])
+    assert np.all(np.isfinite(E)) and E.min() >= 0 and E.max() <= K * (1 + 1e-6)
+    assert rel_err(r["loss"].item(), -E.mean()) <= 1e-6
+    rng = np.random.default_rng(5)
+    idx = np.unique(np.concatenate([[0, N - 1], rng.choice(N, size=8, replace=False)]))
+    sel = torch.as_tensor(idx, device=dev)
+    zd_s, zt_s = host64(zd[sel]), host64(zt[sel])
+    scale = len(idx) / N
+    tol = loss_tol(zd.dtype)
+    if mode == "wtv":
+        o = O.wtv_loss(zd_s, zt_s, 1.0, 1.0)
+        np.testing.assert_allclose(host64(r["accept"][sel]), o["a"], rtol=tol, atol=1e-4)
+        coef = wtv_coef(o, len(idx), 1.0) * scale
+        rows, elems = wtv_flips(zd_s, zt_s, 1.0, 1.0, coef)
+        check_grad(host64(r["grad"][sel]), o["grad"] * scale, coef, zd.dtype, zd.dtype, exclude_rows=rows,
+                   exclude_elems=elems)
+    else:
+        o = O.eal_loss(zd_s, zt_s, 1.0)
+        assert np.array_equal(r["xstar"][sel].cpu().numpy(), o["xstar"])
+        np.testing.assert_allclose(host64(r["accept"][sel]), o["a"], rtol=tol, atol=1e-7)
+        coef = eal_coef(o, len(idx), 1.0) * scale
+        check_grad(host64(r["grad"][sel]), o["grad"] * scale, coef, zd.dtype, zd.dtype)
+    assert rel_err(host64(r["E"][sel]), o["E"]) <= tol
+    del r, inp, zd, zt
+    gc.collect()
+    torch.cuda.empty_cache()
