@@ -29,7 +29,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("aal_eal_fwd_bwd", "aal_wtv_fwd_bwd", "aal_sim_accept_grpo", "aal_workspace_bytes",
               "aal_loss_fwd_bwd", "aal_loss_workspace_bytes", "aal_grpo_fwd_bwd", "aal_grpo_workspace_bytes",
-              "aal_status_string", "aal_last_error", "aal_version"):
+              "aal_status_string", "aal_last_error", "aal_version", "aal_vp_row_partials", "aal_vp_merge_rows",
+              "aal_vp_accept_partials", "aal_vp_window_scan", "aal_vp_grad"):
         assert n in names
 
 
