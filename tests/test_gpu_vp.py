@@ -212,3 +212,10 @@ def test_vp_full_c2_over_8_ranks(A, dev, mode):
     del r, inp, zd, zt
     gc.collect()
     torch.cuda.empty_cache()
+
+
+def test_vp_rows_past_the_grid(A, dev):
+    # more rows than row workgroups launched (65,536): the row kernels visit the rest grid-stride
+    zd, zt = _inputs("c2", (70001, 1, 40), BF16, seed=8, dev=dev)
+    check_eal(A, zd, zt, [16, 24], 1.0, F32)
+    check_wtv(A, zd, zt, [16, 24], 1.0, 1.0, F32)
