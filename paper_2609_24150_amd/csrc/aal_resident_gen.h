@@ -473,7 +473,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
             }
             if constexpr (KL) {
               const float ep = ex2(t);  // p 2^l2s_d; p = 0 contributes nothing
-              sk += (ep > 0.f) ? ep * (t - u) : 0.f;
+              sk = __builtin_fmaf(ep, (ep > 0.f) ? (t - u) : 0.f, sk);
             }
           }
         }
