@@ -98,7 +98,7 @@ def check_wtv(A, zd, zt, widths, Td=1.0, Tt=1.0, gdtype=None, scale=None):
 # (dtype, gdtype, N, K, slice widths): one slice (the whole vocabulary), equal
 # vector-multiple slices, ragged slices that leave the 16-byte vector path,
 # slices narrower than a vector, slices spanning several 256-thread tiles with
-# ragged tails, and one rank's share of a 128,256-entry vocabulary over 8 ranks.
+# ragged tails, and one rank's share of 128,256- and 151,936-entry vocabularies over 8 ranks.
 CASES = [
     (BF16, BF16, 3, 4, [1000]),
     (BF16, BF16, 3, 7, [1024] * 4),
@@ -106,6 +106,7 @@ CASES = [
     (F32, F32, 3, 3, [1, 2, 5, 992]),
     (F32, BF16, 2, 4, [2500, 1599]),
     (BF16, BF16, 2, 7, [16032] * 8),
+    (BF16, BF16, 1, 5, [18992] * 8),
     (F32, F32, 2, 16, [4000] * 8),
 ]
 
