@@ -198,3 +198,22 @@ def test_vp_validation(lib):
     assert G(16, 16, 0, 2, 8, 0, 1, 1.0, 1.0, 16, 16, 9, None) == 2
     assert G(16, 16, 0, 2, 8, 0, 1, 1.0, 1.0, 16, 24, 0, None) == 3
     assert G(16, None, 0, 2, 8, 0, 1, 1.0, 1.0, 16, 16, 0, None) == 1   # WTV reads the target
+
+
+def test_vp_record_layouts_match_the_binding(tmp_path, lib):
+    """The record sizes the Python binding allocates equal the C struct sizes."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include "aal.h"\n'
+        f"_Static_assert(sizeof(aal_vp_part_t) == {lib.VP_PART_BYTES}, \"part\");\n"
+        f"_Static_assert(sizeof(aal_vp_acc_t) == {lib.VP_ACC_BYTES}, \"acc\");\n"
+        f"_Static_assert(sizeof(aal_vp_row_t) == {lib.VP_ROW_BYTES}, \"row\");\n"
+        f"_Static_assert(AAL_VP_EAL == {lib.AAL_VP_EAL} && AAL_VP_WTV == {lib.AAL_VP_WTV}, \"modes\");\n")
+    r = subprocess.run([cc, "-std=c11", "-fsyntax-only", f"-I{os.path.join(ROOT, 'include')}", str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
