@@ -240,8 +240,8 @@ def vp_call(zd_s, zt_s, v0, R, N, K, mode, grad_dtype):
     s = stream.cuda_stream
 
     def fn():
-        _lib.check(L.aal_vp_row_partials(zd_s.data_ptr(), zt_s.data_ptr(), dcode, rows, vs, v0, mode, 1.0, 1.0,
-                                         parts[0].data_ptr(), s), "aal_vp_row_partials")
+        _lib.check(L.aal_vp_row_partials(zd_s.data_ptr(), zt_s.data_ptr(), None, dcode, rows, vs, v0, mode, 1.0,
+                                         1.0, parts[0].data_ptr(), s), "aal_vp_row_partials")
         parts[1:].copy_(parts[0].expand(R - 1, -1, -1))
         _lib.check(L.aal_vp_merge_rows(parts.data_ptr(), R, rows, mode, 1.0, 1.0, row.data_ptr(), s),
                    "aal_vp_merge_rows")

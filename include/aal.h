@@ -335,7 +335,8 @@ typedef enum { AAL_VP_EAL = 0, AAL_VP_WTV = 1 } aal_vp_mode_t;
  *   zd_at          : EAL: the draft logit at t_idx (0 if t_idx is INT32_MAX)
  *   t_idx          : EAL: global index of the slice's largest target logit,
  *                    lowest index on ties, INT32_MAX if the slice has no finite
- *                    target logit; WTV: -1 */
+ *                    target logit (with labels: the row's label if the slice
+ *                    holds it, else INT32_MAX); WTV: -1 */
 typedef struct {
   float zmax_d, s_d, zmax_t, s_t, zd_at;
   int32_t t_idx, reserved0, reserved1;
@@ -365,12 +366,17 @@ typedef struct {
  * Step 1.  z_draft, z_target : [rows, V_slice] of in_dtype, the slice that
  * starts at global vocabulary index v0.  rows >= 1, V_slice >= 1, v0 >= 0,
  * v0 + V_slice < 2^31, rows*V_slice < 2^62.  EAL ignores temp_target.
+ * labels : EAL only, [rows] int32 global token ids that replace the target's
+ *          greedy token (as in aal_loss_fwd_bwd), or NULL.  With labels the
+ *          target logits are not read and z_target may be NULL; the slice
+ *          that holds a row's label supplies its candidate, and a label that
+ *          lies in no slice leaves the row without one (x* = 0, a = 0).
  * parts : [rows] records, required.
  */
-aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
-                                 int64_t rows, int32_t V_slice, int32_t v0, aal_vp_mode_t mode,
-                                 float temp_draft, float temp_target, aal_vp_part_t* parts,
-                                 void* stream);
+aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, const int32_t* labels,
+                                 aal_dtype_t in_dtype, int64_t rows, int32_t V_slice, int32_t v0,
+                                 aal_vp_mode_t mode, float temp_draft, float temp_target,
+                                 aal_vp_part_t* parts, void* stream);
 
 /*
  * Step 2.  parts_all : [R, rows] records, rank-major (rank r's records at

@@ -72,7 +72,7 @@ _SIGNATURES = {
         C.c_int32, _vp, C.c_float, GrpoParams, _vp, _vp, _vp, _vp, _vp,
         _vp, C.c_int, _vp, _vp, C.c_size_t, _vp]),
     "aal_vp_row_partials": (C.c_int, [
-        _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_float, C.c_float, _vp, _vp]),
+        _vp, _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_float, C.c_float, _vp, _vp]),
     "aal_vp_merge_rows": (C.c_int, [_vp, C.c_int32, C.c_int64, C.c_int, C.c_float, C.c_float, _vp, _vp]),
     "aal_vp_accept_partials": (C.c_int, [
         _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_float, C.c_float, _vp, _vp, _vp]),

@@ -287,14 +287,20 @@ def _records(t: torch.Tensor, nbytes: int, name: str, lead: int):
         raise ValueError(f"{name} must be a contiguous uint8 tensor of records of {nbytes} bytes")
 
 
-def aal_vp_row_partials(z_draft: torch.Tensor, z_target: torch.Tensor, v0: int, mode: int,
-                        temp_draft: float = 1.0, temp_target: float = 1.0, *, stream=None) -> torch.Tensor:
-    """Step 1: partial row statistics of the slice [v0, v0 + V_slice).  Returns [rows, 32] records."""
-    rows, vs, dev = _vp_slice(z_draft, z_target)
+def aal_vp_row_partials(z_draft: torch.Tensor, z_target: torch.Tensor | None, v0: int, mode: int,
+                        temp_draft: float = 1.0, temp_target: float = 1.0, *, labels: torch.Tensor | None = None,
+                        stream=None) -> torch.Tensor:
+    """Step 1: partial row statistics of the slice [v0, v0 + V_slice).  EAL may
+    take int32 labels [rows] (global token ids) in place of the target's greedy
+    token; the target slice may then be None.  Returns [rows, 32] records."""
+    rows, vs, dev = _vp_slice(z_draft, z_target, need_target=labels is None)
+    if labels is not None and (labels.dtype != torch.int32 or labels.numel() != rows or labels.device != dev
+                               or not labels.is_contiguous()):
+        raise ValueError("labels must be a contiguous int32 device tensor with one entry per row")
     parts = torch.empty(rows, _lib.VP_PART_BYTES, dtype=torch.uint8, device=dev)
-    st = _lib.lib().aal_vp_row_partials(_ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), rows, vs, int(v0),
-                                        int(mode), float(temp_draft), float(temp_target), _ptr(parts),
-                                        _stream(dev, stream))
+    st = _lib.lib().aal_vp_row_partials(_ptr(z_draft), _ptr(z_target), _ptr(labels), _dtype_code(z_draft.dtype),
+                                        rows, vs, int(v0), int(mode), float(temp_draft), float(temp_target),
+                                        _ptr(parts), _stream(dev, stream))
     _lib.check(st, "aal_vp_row_partials")
     return parts
 

@@ -494,19 +494,24 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
 }
 
 
-aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t rows,
-                                 int32_t V_slice, int32_t v0, aal_vp_mode_t mode, float temp_draft,
-                                 float temp_target, aal_vp_part_t* parts, void* stream) {
+aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, const int32_t* labels,
+                                 aal_dtype_t in_dtype, int64_t rows, int32_t V_slice, int32_t v0,
+                                 aal_vp_mode_t mode, float temp_draft, float temp_target, aal_vp_part_t* parts,
+                                 void* stream) {
   g_last_error.clear();
   if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
-  aal_status_t st = validate_vp_slice(z_draft, z_target, true, int(in_dtype), rows, V_slice, v0);
+  if (labels && mode != AAL_VP_EAL) return fail(AAL_ERR_ARG, "labels are for EAL mode only");
+  if (labels && !aligned(labels, 4)) return fail(AAL_ERR_ALIGN, "labels must be 4-byte aligned");
+  aal_status_t st = validate_vp_slice(z_draft, labels ? nullptr : z_target, !labels, int(in_dtype), rows, V_slice,
+                                      v0);
   if (st != AAL_OK) return st;
   if (!parts) return fail(AAL_ERR_ARG, "parts must be non-NULL");
   if (!aligned(parts, 4)) return fail(AAL_ERR_ALIGN, "parts must be 4-byte aligned");
   aal::VpSlice s{};
   if ((st = vp_scales(int(mode), temp_draft, temp_target, &s.scd, &s.sct)) != AAL_OK) return st;
   s.zd = z_draft;
-  s.zt = z_target;
+  s.zt = labels ? nullptr : z_target;
+  s.labels = labels;
   s.in = to_dtype(in_dtype);
   s.rows = rows;
   s.vs = V_slice;

@@ -11,6 +11,7 @@ namespace aal {
 struct VpSlice {
   const void* zd;
   const void* zt;
+  const int32_t* labels;  // EAL: [rows] global token ids replacing the greedy token, or null
   DType in;
   int64_t rows;
   int32_t vs;    // V_slice

@@ -35,9 +35,12 @@ constexpr int kMaxRowBlocks = 65536;  // rows beyond this are visited grid-strid
 
 unsigned row_grid(int64_t rows) { return unsigned(rows < kMaxRowBlocks ? rows : kMaxRowBlocks); }
 
-template <class TI, int MODE, bool VEC, int U>
+// LAB (EAL with labels): the label replaces the greedy token and the target
+// slice is not read.
+template <class TI, int MODE, bool VEC, int U, bool LAB>
 __global__ __launch_bounds__(kBlock) void k_vp_partials(const void* __restrict__ zd, const void* __restrict__ zt,
-                                                        int64_t rows, int Vs, int v0, float scd, float sct,
+                                                        const int32_t* __restrict__ labels, int64_t rows, int Vs,
+                                                        int v0, float scd, float sct,
                                                         aal_vp_part_t* __restrict__ parts) {
   using Gr = Groups<TI, VEC>;
   constexpr int E = Gr::E;
@@ -58,7 +61,7 @@ __global__ __launch_bounds__(kBlock) void k_vp_partials(const void* __restrict__
         const int gi = base + u * kBlock;
         if (gi < ng) {
           Gr::load(zd, g0, gi, xd[u]);
-          Gr::load(zt, g0, gi, xt[u]);
+          if constexpr (!LAB) Gr::load(zt, g0, gi, xt[u]);
         } else {
 #pragma unroll
           for (int e = 0; e < E; ++e) xd[u][e] = xt[u][e] = kNegInf;
@@ -91,7 +94,7 @@ __global__ __launch_bounds__(kBlock) void k_vp_partials(const void* __restrict__
             for (int e = 0; e < E; ++e) acc += ex2(__builtin_fmaf(xt[u][e], sct, -st.msc));
           st.s += acc;
         }
-      } else {
+      } else if constexpr (!LAB) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -108,7 +111,19 @@ __global__ __launch_bounds__(kBlock) void k_vp_partials(const void* __restrict__
     out.s_d = sd.s;
     out.reserved0 = 0;
     out.reserved1 = 0;
-    if constexpr (MODE == int(Mode::kEal)) {
+    if constexpr (LAB) {
+      const int64_t xl = int64_t(labels[row]) - v0;  // the label in slice coordinates
+      if (xl >= 0 && xl < Vs) {
+        out.zmax_t = 0.f;  // the only candidate of the row: its value decides nothing
+        out.zd_at = TI::load1(zd, row * int64_t(Vs) + xl);
+        out.t_idx = int(xl) + v0;
+      } else {
+        out.zmax_t = kNegInf;
+        out.zd_at = 0.f;
+        out.t_idx = INT_MAX;
+      }
+      out.s_t = 0.f;
+    } else if constexpr (MODE == int(Mode::kEal)) {
       const int x = block_argmax(best, bidx, sh_f, sh_i);
       const int64_t e0 = row * int64_t(Vs);
       if (x == INT_MAX) {
@@ -330,15 +345,26 @@ __global__ __launch_bounds__(kBlock) void k_vp_grad(const void* __restrict__ zd,
   }
 }
 
-template <class TI, int MODE>
-void partials_typed(const VpSlice& s, aal_vp_part_t* parts) {
+template <class TI, int MODE, bool LAB>
+void partials_lab(const VpSlice& s, aal_vp_part_t* parts) {
   const unsigned grid = row_grid(s.rows);
   if (s.vs % TI::kVec == 0)
-    k_vp_partials<TI, MODE, true, 4><<<grid, kBlock, 0, s.stream>>>(s.zd, s.zt, s.rows, s.vs, s.v0, s.scd, s.sct,
-                                                                     parts);
+    k_vp_partials<TI, MODE, true, 4, LAB><<<grid, kBlock, 0, s.stream>>>(s.zd, s.zt, s.labels, s.rows, s.vs, s.v0,
+                                                                          s.scd, s.sct, parts);
   else
-    k_vp_partials<TI, MODE, false, 8><<<grid, kBlock, 0, s.stream>>>(s.zd, s.zt, s.rows, s.vs, s.v0, s.scd, s.sct,
-                                                                      parts);
+    k_vp_partials<TI, MODE, false, 8, LAB><<<grid, kBlock, 0, s.stream>>>(s.zd, s.zt, s.labels, s.rows, s.vs, s.v0,
+                                                                           s.scd, s.sct, parts);
+}
+
+template <class TI, int MODE>
+void partials_typed(const VpSlice& s, aal_vp_part_t* parts) {
+  if constexpr (MODE == int(Mode::kEal)) {
+    if (s.labels) {
+      partials_lab<TI, MODE, true>(s, parts);
+      return;
+    }
+  }
+  partials_lab<TI, MODE, false>(s, parts);
 }
 
 template <class TI>

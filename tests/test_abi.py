@@ -168,13 +168,14 @@ def test_vp_validation(lib):
     L = lib.lib()
     P = L.aal_vp_row_partials
 
-    def part(zd=16, zt=16, dt=0, rows=2, vs=8, v0=0, mode=0, td=1.0, tt=1.0, parts=16):
-        return P(zd, zt, dt, rows, vs, v0, mode, td, tt, parts, None)
+    def part(zd=16, zt=16, lab=None, dt=0, rows=2, vs=8, v0=0, mode=0, td=1.0, tt=1.0, parts=16):
+        return P(zd, zt, lab, dt, rows, vs, v0, mode, td, tt, parts, None)
 
     for kw, code in [(dict(rows=0), 1), (dict(vs=0), 1), (dict(v0=-1), 1), (dict(v0=(1 << 31) - 4), 1),
                      (dict(dt=5), 2), (dict(zd=18), 3), (dict(zt=None), 1), (dict(mode=9), 1),
                      (dict(mode=1, tt=0.0), 1), (dict(td=float("nan")), 1), (dict(parts=None), 1),
-                     (dict(parts=18), 3), (dict(rows=1 << 60), 1)]:
+                     (dict(parts=18), 3), (dict(rows=1 << 60), 1), (dict(lab=16, mode=1), 1),
+                     (dict(lab=18), 3), (dict(lab=16, zd=None), 1)]:
         assert part(**kw) == code, kw
         assert L.aal_last_error().decode() != ""
     M = L.aal_vp_merge_rows

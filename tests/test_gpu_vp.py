@@ -44,13 +44,14 @@ def _bounds(V, widths):
     return [(int(a), int(w)) for a, w in zip(v0, widths)]
 
 
-def run_vp(A, zd, zt, mode, widths, Td=1.0, Tt=1.0, gdtype=None, scale=None):
+def run_vp(A, zd, zt, mode, widths, Td=1.0, Tt=1.0, gdtype=None, scale=None, labels=None):
     """The five steps over slices of the given widths; returns the fused calls' outputs."""
     N, K, V = zd.shape
     rows = N * K
     sl = [(v0, w, zd.reshape(rows, V)[:, v0:v0 + w].contiguous(), zt.reshape(rows, V)[:, v0:v0 + w].contiguous())
           for v0, w in _bounds(V, widths)]
-    parts = torch.stack([A.aal_vp_row_partials(d, t, v0, mode, Td, Tt) for v0, w, d, t in sl])
+    parts = torch.stack([A.aal_vp_row_partials(d, None if labels is not None else t, v0, mode, Td, Tt, labels=labels)
+                         for v0, w, d, t in sl])
     row = A.aal_vp_merge_rows(parts, mode, Td, Tt)
     acc = None
     if mode == A.AAL_VP_WTV:
@@ -220,3 +221,23 @@ def test_vp_rows_past_the_grid(A, dev):
     zd, zt = _inputs("c2", (70001, 1, 40), BF16, seed=8, dev=dev)
     check_eal(A, zd, zt, [16, 24], 1.0, F32)
     check_wtv(A, zd, zt, [16, 24], 1.0, 1.0, F32)
+
+
+@pytest.mark.parametrize("dtype,widths", [(BF16, [1024] * 4), (F32, [300, 301, 399]), (BF16, [16032] * 8)])
+def test_vp_eal_labels(A, dev, dtype, widths):
+    """Labels replace the greedy token (the target slices are not read); against
+    the oracle's EAL term with labels."""
+    N, K, V = 3, 5, sum(widths)
+    zd, zt = _inputs("c2", (N, K, V), dtype, seed=17, dev=dev)
+    g = torch.Generator().manual_seed(3)
+    lab = torch.randint(0, V, (N * K,), generator=g, dtype=torch.int32)
+    lab[0] = 0
+    lab[-1] = V - 1
+    r = run_vp(A, zd, zt, A.AAL_VP_EAL, widths, 0.8, 1.0, F32, labels=lab.to(dev))
+    o = O.combined_loss(host64(zd), host64(zt), 0.8, 1.0, (0.0, 1.0, 0.0, 0.0), 0, N, K, K, labels=lab.numpy())
+    assert np.array_equal(r["xstar"].cpu().numpy().reshape(-1), lab.numpy())
+    tol = loss_tol(zd.dtype)
+    assert rel_err(r["loss"].item(), o["loss"]) <= tol
+    assert rel_err(host64(r["E"]), o["E_eal"]) <= tol
+    np.testing.assert_allclose(host64(r["accept"]).reshape(-1), o["a_eal"], rtol=tol, atol=1e-7)
+    check_grad(host64(r["grad"]), o["grad"], o["coef_eal"], zd.dtype, F32)
