@@ -410,6 +410,25 @@ aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, 
                                 float* accept, int32_t* target_argmax, void* stream);
 
 /*
+ * Step 4 for sequences (the layout of aal_loss_fwd_bwd with
+ * AAL_LAYOUT_SEQUENCES): the N*K rows are B sequences of S positions, and a
+ * window of K positions starts at every position t <= S - K of a sequence
+ * (windows sliding by one, Section "Window TV Loss"); W = B (S - K + 1).
+ *   loss = -(1/W) sum_windows E_w, and each row's coefficient sums dE_w/da
+ *   over the (at most K) windows that contain it.
+ * row : [B*S] records from step 2, updated in place as in aal_vp_window_scan.
+ * acc_all : [R, B*S] (WTV), as there.  B >= 1, 1 <= K <= 64, K <= S,
+ * B*S < 2^31.  loss [1] and eal_per_window [W] (window t of sequence b at
+ * b (S - K + 1) + t) are required; accept [B*S] and target_argmax [B*S] (EAL)
+ * may be NULL.
+ */
+aal_status_t aal_vp_sequence_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R,
+                                  int64_t B, int32_t S, int32_t K, aal_vp_mode_t mode,
+                                  float temp_draft, const float* grad_scale, float* loss,
+                                  float* eal_per_window, float* accept, int32_t* target_argmax,
+                                  void* stream);
+
+/*
  * Step 5.  The slice as in step 1 (EAL reads only z_draft; z_target may then be
  * NULL), row from step 4.  grad_draft : [rows, V_slice] of grad_dtype, the
  * slice of the gradient of the loss, times *grad_scale as folded into coef.

@@ -22,6 +22,7 @@ from .api import (  # noqa: F401
     aal_vp_grad,
     aal_vp_merge_rows,
     aal_vp_row_partials,
+    aal_vp_sequence_scan,
     aal_vp_window_scan,
     aal_workspace_bytes,
     aal_wtv_fwd_bwd,

@@ -78,6 +78,8 @@ _SIGNATURES = {
         _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_float, C.c_float, _vp, _vp, _vp]),
     "aal_vp_window_scan": (C.c_int, [
         _vp, _vp, C.c_int32, C.c_int64, C.c_int32, C.c_int, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "aal_vp_sequence_scan": (C.c_int, [
+        _vp, _vp, C.c_int32, C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp]),
     "aal_vp_grad": (C.c_int, [
         _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_float, C.c_float, _vp, _vp, C.c_int,
         _vp]),

@@ -366,6 +366,39 @@ def aal_vp_window_scan(row: torch.Tensor, acc_all: torch.Tensor | None, N: int, 
     return out
 
 
+def aal_vp_sequence_scan(row: torch.Tensor, acc_all: torch.Tensor | None, B: int, S: int, K: int, mode: int,
+                         temp_draft: float = 1.0, *, grad_scale: torch.Tensor | None = None, stream=None) -> dict:
+    """Step 4 for B sequences of S positions with windows of K sliding by one
+    (rows updated in place).  Returns loss [1], E [B*(S-K+1)], accept [B, S]
+    and, in EAL mode, xstar [B, S]."""
+    _records(row, _lib.VP_ROW_BYTES, "row", 1)
+    if row.shape[0] != B * S:
+        raise ValueError("row must hold B*S records")
+    dev = row.device
+    R = 0
+    if mode == _lib.AAL_VP_WTV:
+        if acc_all is None:
+            raise ValueError("acc_all is required in WTV mode")
+        _records(acc_all, _lib.VP_ACC_BYTES, "acc_all", 2)
+        if acc_all.shape[1] != B * S:
+            raise ValueError("acc_all must be [R, B*S, 8]")
+        R = acc_all.shape[0]
+    if grad_scale is not None and (grad_scale.dtype != torch.float32 or grad_scale.device != dev):
+        raise TypeError("grad_scale must be a float32 device tensor")
+    out = {
+        "loss": torch.empty(1, dtype=torch.float32, device=dev),
+        "E": torch.empty(B * max(0, S - K + 1), dtype=torch.float32, device=dev),
+        "accept": torch.empty(B, S, dtype=torch.float32, device=dev),
+    }
+    if mode == _lib.AAL_VP_EAL:
+        out["xstar"] = torch.empty(B, S, dtype=torch.int32, device=dev)
+    st = _lib.lib().aal_vp_sequence_scan(_ptr(row), _ptr(acc_all) if R else None, R, B, S, K, int(mode),
+                                         float(temp_draft), _ptr(grad_scale), _ptr(out["loss"]), _ptr(out["E"]),
+                                         _ptr(out["accept"]), _ptr(out.get("xstar")), _stream(dev, stream))
+    _lib.check(st, "aal_vp_sequence_scan")
+    return out
+
+
 def aal_vp_grad(z_draft: torch.Tensor, z_target: torch.Tensor | None, row: torch.Tensor, v0: int, mode: int,
                 temp_draft: float = 1.0, temp_target: float = 1.0, *, grad_dtype: torch.dtype | None = None,
                 stream=None) -> torch.Tensor:

@@ -588,6 +588,33 @@ aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, 
   return AAL_OK;
 }
 
+aal_status_t aal_vp_sequence_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R, int64_t B, int32_t S,
+                                  int32_t K, aal_vp_mode_t mode, float temp_draft, const float* grad_scale,
+                                  float* loss, float* eal_per_window, float* accept, int32_t* target_argmax,
+                                  void* stream) {
+  g_last_error.clear();
+  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
+  if (!row || !loss || !eal_per_window) return fail(AAL_ERR_ARG, "row, loss and eal_per_window must be non-NULL");
+  if (B < 1) return fail(AAL_ERR_ARG, "B must be >= 1 (got %lld)", (long long)B);
+  if (K < 1 || K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", K);
+  if (S < K) return fail(AAL_ERR_ARG, "S must be >= K (got S = %d, K = %d)", S, K);
+  if (B > (int64_t(1) << 31) / S) return fail(AAL_ERR_ARG, "B*S must be < 2^31");
+  const bool wtv = mode == AAL_VP_WTV;
+  if (wtv && !acc_all) return fail(AAL_ERR_ARG, "acc_all must be non-NULL in WTV mode");
+  if (wtv && R < 1) return fail(AAL_ERR_ARG, "R must be >= 1 (got %d)", R);
+  if (wtv && B * S > (int64_t(1) << 56) / R) return fail(AAL_ERR_ARG, "R*B*S must be < 2^56");
+  if (!aligned(row, 4) || (wtv && !aligned(acc_all, 4))) return fail(AAL_ERR_ALIGN, "records must be 4-byte aligned");
+  float scd, sct;
+  aal_status_t st = vp_scales(AAL_VP_EAL, temp_draft, 1.f, &scd, &sct);
+  if (st != AAL_OK) return st;
+  const hipError_t e = aal::launch_vp_seq_scan(row, wtv ? acc_all : nullptr, wtv ? R : 0, B, S, K,
+                                               vp_mode(int(mode)), 1.0f / temp_draft, grad_scale, loss,
+                                               eal_per_window, accept, wtv ? nullptr : target_argmax,
+                                               static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
 aal_status_t aal_vp_grad(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t rows,
                          int32_t V_slice, int32_t v0, aal_vp_mode_t mode, float temp_draft, float temp_target,
                          const aal_vp_row_t* row, void* grad_draft, aal_dtype_t grad_dtype, void* stream) {

@@ -28,6 +28,9 @@ hipError_t launch_vp_accept(const VpSlice& s, const aal_vp_row_t* row, aal_vp_ac
 hipError_t launch_vp_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R, int64_t N, int32_t K, Mode mode,
                           float inv_t_d, const float* grad_scale, float* loss, float* window_e, float* accept,
                           int32_t* xstar, hipStream_t stream);
+hipError_t launch_vp_seq_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R, int64_t B, int32_t S,
+                              int32_t K, Mode mode, float inv_t_d, const float* grad_scale, float* loss,
+                              float* window_e, float* accept, int32_t* xstar, hipStream_t stream);
 hipError_t launch_vp_grad(const VpSlice& s, const aal_vp_row_t* row, void* grad, DType gd);
 
 }  // namespace aal

@@ -14,6 +14,8 @@
 //                  then prefix products, E = sum_k P_k (Eq. eal_generic) and
 //                  the coefficients dloss/da_j = -P_j S_j / N (Eqs. loss_eal,
 //                  loss_tv); the loss is reduced afterwards in fixed order.
+//   k_vp_seq_scan  the same for sequences with windows sliding by one: one
+//                  thread per row sums dE/da over the windows that contain it.
 //   k_vp_grad      one workgroup per row: the slice of dloss/dz_draft.
 //
 // A slice is HBM-bound like the streaming schedule it mirrors: the partial
@@ -296,6 +298,67 @@ __global__ __launch_bounds__(kBlock) void k_vp_scan(aal_vp_row_t* __restrict__ r
   window_e[n] = float(E);
 }
 
+// WTV before a sequence scan: each row's acceptance partials summed in rank
+// order (a row's coefficient needs its neighbours' sums).
+__global__ __launch_bounds__(kBlock) void k_vp_merge_acc(aal_vp_row_t* __restrict__ rec,
+                                                         const aal_vp_acc_t* __restrict__ acc, int R,
+                                                         int64_t rows) {
+  const int64_t r = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (r >= rows) return;
+  float a = 0.f, q = 0.f;
+  for (int k = 0; k < R; ++k) {
+    const aal_vp_acc_t& p = acc[int64_t(k) * rows + r];
+    a += p.smin;
+    q += p.qlt;
+  }
+  rec[r].a = a;
+  rec[r].qlt = q;
+}
+
+// dE/da_j of the window whose rows start at r0: P_j S_j with
+// P_j = prod_{i<j} a_i, S_{K-1} = 1, S_i = 1 + a_{i+1} S_{i+1} (fp64).
+__device__ double window_dE_vp(const aal_vp_row_t* __restrict__ rec, int64_t r0, int K, int j) {
+  double P = 1.0;
+  for (int i = 0; i < j; ++i) P *= double(rec[r0 + i].a);
+  double S = 1.0;
+  for (int i = K - 1; i > j; --i) S = 1.0 + double(rec[r0 + i].a) * S;
+  return P * S;
+}
+
+// One thread per row of B sequences of S positions with windows of K
+// positions sliding by one: the row's coefficient sums dE/da over the windows
+// that contain it; the row that starts a window also writes that window's E.
+__global__ __launch_bounds__(kBlock) void k_vp_seq_scan(aal_vp_row_t* __restrict__ rec, int64_t B, int S, int K,
+                                                        int mode, float inv_t_d, const float* __restrict__ grad_scale,
+                                                        float* __restrict__ window_e, float* __restrict__ accept,
+                                                        int32_t* __restrict__ xstar) {
+  const int64_t r = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (r >= B * S) return;
+  const int64_t b = r / S;
+  const int64_t base = b * S;
+  const int s = int(r - base);
+  const int t0 = s - K + 1 > 0 ? s - K + 1 : 0;
+  const int t1 = s < S - K ? s : S - K;
+  double d = 0.0;
+  for (int t = t0; t <= t1; ++t) d += window_dE_vp(rec, base + t, K, s - t);
+  const double W = double(B) * double(S - K + 1);
+  const double scale = grad_scale ? double(*grad_scale) : 1.0;
+  const float a = rec[r].a;
+  const double factor = (mode == int(Mode::kEal)) ? double(a) * double(inv_t_d) : double(inv_t_d);
+  if (s <= S - K) {  // this row starts window s of its sequence
+    double p = 1.0, E = 0.0;
+    for (int j = 0; j < K; ++j) {
+      p *= double(rec[r + j].a);
+      E += p;
+    }
+    window_e[b * (S - K + 1) + s] = float(E);
+  }
+  if (accept) accept[r] = a;
+  if (xstar) xstar[r] = rec[r].xstar;
+  // written last: other threads read only a of this row
+  rec[r].coef = float(-d / W * scale * factor);
+}
+
 template <class TI, class TG, int MODE, bool VEC, int U>
 __global__ __launch_bounds__(kBlock) void k_vp_grad(const void* __restrict__ zd, const void* __restrict__ zt,
                                                     int64_t rows, int Vs, int v0, float scd, float sct,
@@ -433,6 +496,24 @@ hipError_t launch_vp_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_
   LossArgs a{};
   a.window_e = window_e;
   a.N = N;
+  a.loss = loss;
+  a.stream = stream;
+  return launch_loss_reduce(a);
+}
+
+hipError_t launch_vp_seq_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R, int64_t B, int32_t S,
+                              int32_t K, Mode mode, float inv_t_d, const float* grad_scale, float* loss,
+                              float* window_e, float* accept, int32_t* xstar, hipStream_t stream) {
+  const int64_t rows = B * S;
+  const unsigned blocks = unsigned((rows + kBlock - 1) / kBlock);
+  if (mode == Mode::kWtv) k_vp_merge_acc<<<blocks, kBlock, 0, stream>>>(row, acc_all, R, rows);
+  k_vp_seq_scan<<<blocks, kBlock, 0, stream>>>(row, B, S, K, int(mode), inv_t_d, grad_scale, window_e, accept,
+                                               xstar);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  LossArgs a{};
+  a.window_e = window_e;
+  a.N = B * int64_t(S - K + 1);
   a.loss = loss;
   a.stream = stream;
   return launch_loss_reduce(a);

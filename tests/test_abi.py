@@ -30,7 +30,7 @@ def test_header_declares_the_boundary():
     for n in ("aal_eal_fwd_bwd", "aal_wtv_fwd_bwd", "aal_sim_accept_grpo", "aal_workspace_bytes",
               "aal_loss_fwd_bwd", "aal_loss_workspace_bytes", "aal_grpo_fwd_bwd", "aal_grpo_workspace_bytes",
               "aal_status_string", "aal_last_error", "aal_version", "aal_vp_row_partials", "aal_vp_merge_rows",
-              "aal_vp_accept_partials", "aal_vp_window_scan", "aal_vp_grad"):
+              "aal_vp_accept_partials", "aal_vp_window_scan", "aal_vp_sequence_scan", "aal_vp_grad"):
         assert n in names
 
 
@@ -194,6 +194,13 @@ def test_vp_validation(lib):
     assert S(16, 16, 1, 2, 3, 0, 1.0, None, None, 16, None, None, None) == 1
     assert S(16, 16, 1, 2, 3, 0, 1.0, None, 16, None, None, None, None) == 1
     assert S(16, 16, 1, 2, 3, 0, 0.0, None, 16, 16, None, None, None) == 1
+    Q = L.aal_vp_sequence_scan
+    assert Q(16, 16, 1, 2, 5, 7, 0, 1.0, None, 16, 16, None, None, None) == 1   # S < K
+    assert Q(16, 16, 1, 0, 8, 7, 0, 1.0, None, 16, 16, None, None, None) == 1   # B = 0
+    assert Q(16, None, 1, 2, 8, 7, 1, 1.0, None, 16, 16, None, None, None) == 1  # WTV needs acc_all
+    assert Q(16, 16, 1, 2, 8, 65, 0, 1.0, None, 16, 16, None, None, None) == 1
+    assert Q(16, 16, 1, 2, 8, 7, 0, 1.0, None, 16, None, None, None, None) == 1
+    assert Q(16, 16, 1, 2, 8, 7, 5, 1.0, None, 16, 16, None, None, None) == 1
     G = L.aal_vp_grad
     assert G(16, 16, 0, 2, 8, 0, 1, 1.0, 1.0, 16, None, 0, None) == 1
     assert G(16, 16, 0, 2, 8, 0, 1, 1.0, 1.0, 16, 16, 9, None) == 2

@@ -241,3 +241,59 @@ def test_vp_eal_labels(A, dev, dtype, widths):
     assert rel_err(host64(r["E"]), o["E_eal"]) <= tol
     np.testing.assert_allclose(host64(r["accept"]).reshape(-1), o["a_eal"], rtol=tol, atol=1e-7)
     check_grad(host64(r["grad"]), o["grad"], o["coef_eal"], zd.dtype, F32)
+
+
+def run_vp_seq(A, zd, zt, mode, widths, K, Td=1.0, Tt=1.0, gdtype=None, scale=None):
+    """The vocabulary-parallel steps over B sequences [B, S, V] with windows sliding by one."""
+    B, S, V = zd.shape
+    rows = B * S
+    sl = [(v0, w, zd.reshape(rows, V)[:, v0:v0 + w].contiguous(), zt.reshape(rows, V)[:, v0:v0 + w].contiguous())
+          for v0, w in _bounds(V, widths)]
+    parts = torch.stack([A.aal_vp_row_partials(d, t, v0, mode, Td, Tt) for v0, w, d, t in sl])
+    row = A.aal_vp_merge_rows(parts, mode, Td, Tt)
+    acc = None
+    if mode == A.AAL_VP_WTV:
+        acc = torch.stack([A.aal_vp_accept_partials(d, t, row, Td, Tt) for v0, w, d, t in sl])
+    gs = None if scale is None else torch.tensor([scale], device=zd.device)
+    r = A.aal_vp_sequence_scan(row, acc, B, S, K, mode, Td, grad_scale=gs)
+    g = [A.aal_vp_grad(d, t if mode == A.AAL_VP_WTV else None, row, v0, mode, Td, Tt, grad_dtype=gdtype)
+         for v0, w, d, t in sl]
+    r["grad"] = torch.cat(g, dim=1).reshape(B, S, V)
+    torch.cuda.synchronize()
+    return r
+
+
+SEQ_CASES = [
+    ("wtv", BF16, 3, 20, 7, [1024] * 4),
+    ("eal", BF16, 3, 20, 7, [1024] * 4),
+    ("wtv", F32, 2, 9, 3, [300, 301, 399]),
+    ("eal", F32, 2, 5, 5, [500, 500]),
+    ("wtv", BF16, 2, 40, 7, [16032] * 8),
+]
+
+
+@pytest.mark.parametrize("mode,dtype,B,S,K,widths", SEQ_CASES)
+def test_vp_sequences(A, dev, mode, dtype, B, S, K, widths):
+    """Windows sliding over sequences (K <= S, down to one window per sequence)
+    against the oracle's sequence-layout objective with that single term."""
+    V = sum(widths)
+    zd, zt = _inputs("c2" if dtype == BF16 else "c4", (B, S, V), dtype, seed=B * S + K, dev=dev)
+    Td, Tt, scale = 0.9, 1.1, 0.5
+    m = A.AAL_VP_WTV if mode == "wtv" else A.AAL_VP_EAL
+    r = run_vp_seq(A, zd, zt, m, widths, K, Td, Tt, F32, scale)
+    zd64, zt64 = host64(zd), host64(zt)
+    w = (1.0, 0.0, 0.0, 0.0) if mode == "wtv" else (0.0, 1.0, 0.0, 0.0)
+    o = O.combined_loss(zd64, zt64, Td, Tt, w, O.LAYOUT_SEQUENCES, B, S, K, grad_scale=scale)
+    tol = loss_tol(zd.dtype)
+    assert rel_err(r["loss"].item(), o["loss"]) <= tol
+    key = "tv" if mode == "wtv" else "eal"
+    assert rel_err(host64(r["E"]), o["E_" + key]) <= tol
+    atol = (1e-6 if dtype == F32 else 1e-4) if mode == "wtv" else 1e-7
+    np.testing.assert_allclose(host64(r["accept"]).reshape(-1), o["a_" + key], rtol=tol, atol=atol)
+    coef = o["coef_" + key]
+    if mode == "wtv":
+        rows, elems = wtv_flips(zd64, zt64, Td, Tt, coef.reshape(B, S))
+        check_grad(host64(r["grad"]), o["grad"], coef, zd.dtype, F32, exclude_rows=rows, exclude_elems=elems)
+    else:
+        assert np.array_equal(r["xstar"].cpu().numpy().reshape(-1), o["xstar"])
+        check_grad(host64(r["grad"]), o["grad"], coef, zd.dtype, F32)
