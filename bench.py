@@ -31,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+HOST_CPU_SHARE = 16
 PMC_PROFILE = os.path.join(ROOT, "profiles", "resident_wtv_c2_pmc.txt")
 KERNEL_SOURCES = ["paper_2609_24150_amd/csrc/aal_resident.hip", "paper_2609_24150_amd/csrc/aal_resident_common.h",
                   "paper_2609_24150_amd/csrc/aal_device.h", "paper_2609_24150_amd/csrc/aal_internal.h"]
@@ -72,7 +73,8 @@ def cpu_baseline(workload: str, budget_s: float = 12.0) -> dict:
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
         cores = os.cpu_count() or 1
-    workers = max(1, min(16, cores))
+    # one GPU's share of the host is 16 CPUs, whatever the affinity mask shows
+    workers = max(1, min(HOST_CPU_SHARE, cores))
     nwin = 2
     ctx = mp.get_context("fork")
     t0 = time.perf_counter()
@@ -84,7 +86,19 @@ def cpu_baseline(workload: str, budget_s: float = 12.0) -> dict:
     rate = sum(r[0] / r[1] for r in res)
     return {"value": rate, "unit": "logit rows/s", "cores": workers, "kind": "oracle",
             "sample": f"{workers} processes x {nwin} windows of the workload (K={K}, V={V}), each repeated "
-                      f"for ~{budget_s:.0f}s; {rows} rows in {wall:.1f}s wall"}
+                      f"for ~{budget_s:.0f}s; {rows} rows in {wall:.1f}s wall",
+            "rows_per_s_per_core": rate / workers, "affinity_cores": cores,
+            "worker_cap": f"{HOST_CPU_SHARE} (the host CPU share of one GPU)", "cpu_model": _cpu_model()}
+
+
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def measured_traffic(workload: str):
@@ -123,7 +137,59 @@ def _time_calls(fn, steps, warmup, stream):
     return start.elapsed_time(stop) / steps  # ms per call
 
 
-def loss_call(op, inp, grad_dtype, flags=0):
+def _fail(msg):
+    print(f"bench.py: invalid measurement: {msg}", file=sys.stderr)
+    sys.exit(3)
+
+
+def check_outputs(fn, outs, name, e_max=None):
+    """The timed calls left their results in `outs`; one more untimed call
+    must reproduce them bit for bit (the kernels are deterministic), the loss
+    must be finite (a poll time-out of a resident kernel makes it NaN) and
+    every per-window expectation must lie in [0, K]."""
+    import torch
+    torch.cuda.synchronize()
+    first = {k: v.clone() for k, v in outs.items() if v is not None}
+    fn()
+    torch.cuda.synchronize()
+    loss = outs["loss"].item() if "loss" in outs else None
+    if loss is not None and (loss != loss or abs(loss) == float("inf")):
+        _fail(f"{name}: loss is {loss}")
+    for k, v in first.items():
+        if not torch.equal(v.view(torch.uint8) if v.dtype != torch.uint8 else v,
+                           outs[k].view(torch.uint8) if outs[k].dtype != torch.uint8 else outs[k]):
+            _fail(f"{name}: output {k} differs between two identical calls")
+    if e_max is not None and "E" in outs:
+        E = outs["E"]
+        if not bool(torch.isfinite(E).all()) or E.min().item() < 0 or E.max().item() > e_max * (1 + 1e-6):
+            _fail(f"{name}: E outside [0, {e_max}]")
+    return {"loss": loss, "repeat_bitwise_equal": True}
+
+
+def ceilings(dev, nbytes=1 << 32):
+    """Practical HBM ceilings on this GPU from plain device kernels (torch's
+    copy, a two-input elementwise add, a full-tensor sum), each timed with HIP
+    events over 10 launches after 3 warm-up launches."""
+    import torch
+    n = nbytes // 2
+    a = torch.ones(n, dtype=torch.bfloat16, device=dev)
+    b = torch.ones(n, dtype=torch.bfloat16, device=dev)
+    c = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    st = torch.cuda.current_stream(dev)
+    legs = {"read (sum of one bf16 tensor)": (lambda: torch.sum(a, dtype=torch.float32), nbytes),
+            "copy (1 read, 1 write)": (lambda: c.copy_(a), 2 * nbytes),
+            "2 reads, 1 write (a + b)": (lambda: torch.add(a, b, out=c), 3 * nbytes)}
+    res = {}
+    for name, (fn, by) in legs.items():
+        ms = _time_calls(fn, 10, 3, st)
+        res[name] = {"GBps": by / (ms * 1e-3) / 1e9, "frac_of_peak": by / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                     "bytes": by}
+    del a, b, c
+    _free_gpu(torch)
+    return res
+
+
+def loss_call(op, inp, grad_dtype, flags=0, temp_draft=None):
     """A zero-allocation closure over the C entry point with preallocated outputs."""
     import torch
 
@@ -149,20 +215,27 @@ def loss_call(op, inp, grad_dtype, flags=0):
             Td, Tt = cfg.get("temp_draft", 1.0), cfg.get("temp_target", 1.0)
 
         def fn():
-            st = L.aal_wtv_fwd_bwd(zd.data_ptr(), zt.data_ptr(), dcode, N, K, V, Td, Tt, loss.data_ptr(),
-                                   E.data_ptr(), acc.data_ptr(), grad.data_ptr(), gcode, None, flags,
-                                   ws.data_ptr(), ws.numel(), stream.cuda_stream)
+            head = (zd.data_ptr(), zt.data_ptr(), dcode, N, K, V, Td, Tt, loss.data_ptr(), E.data_ptr(),
+                    acc.data_ptr(), grad.data_ptr(), gcode, None)
+            if flags:
+                st = L.aal_wtv_fwd_bwd_ex(*head, flags, ws.data_ptr(), ws.numel(), stream.cuda_stream)
+            else:
+                st = L.aal_wtv_fwd_bwd(*head, ws.data_ptr(), ws.numel(), stream.cuda_stream)
             _lib.check(st, "aal_wtv_fwd_bwd")
     else:
         xs = torch.empty(N, K, dtype=torch.int32, device=dev)
-        Td = cfg.get("temp_draft", 1.0)
+        Td = cfg.get("temp_draft", 1.0) if temp_draft is None else temp_draft
 
         def fn():
-            st = L.aal_eal_fwd_bwd(zd.data_ptr(), zt.data_ptr(), dcode, N, K, V, Td, loss.data_ptr(),
-                                   E.data_ptr(), acc.data_ptr(), xs.data_ptr(), grad.data_ptr(), gcode, None,
-                                   flags, ws.data_ptr(), ws.numel(), stream.cuda_stream)
+            head = (zd.data_ptr(), zt.data_ptr(), dcode, N, K, V, Td, loss.data_ptr(), E.data_ptr(),
+                    acc.data_ptr(), xs.data_ptr(), grad.data_ptr(), gcode, None)
+            if flags:
+                st = L.aal_eal_fwd_bwd_ex(*head, flags, ws.data_ptr(), ws.numel(), stream.cuda_stream)
+            else:
+                st = L.aal_eal_fwd_bwd(*head, ws.data_ptr(), ws.numel(), stream.cuda_stream)
             _lib.check(st, "aal_eal_fwd_bwd")
-    return fn, stream, {"loss": loss, "E": E, "grad": grad}
+        return fn, stream, {"loss": loss, "E": E, "accept": acc, "xstar": xs, "grad": grad}
+    return fn, stream, {"loss": loss, "E": E, "accept": acc, "grad": grad}
 
 
 def sim_call(inp):
@@ -174,7 +247,6 @@ def sim_call(inp):
     P, G, K, V = zd.shape
     dev = zd.device
     tok = torch.empty(P, G, K, dtype=torch.int32, device=dev)
-    acc = torch.empty_like(tok)
     rew = torch.empty(P, G, dtype=torch.int32, device=dev)
     adv = torch.empty(P, G, device=dev)
     ws = A.workspace(P * G * K, P * G, dev)
@@ -184,10 +256,10 @@ def sim_call(inp):
 
     def fn():
         st = L.aal_sim_accept_grpo(zd.data_ptr(), zt.data_ptr(), dcode, P, G, K, V, 1.0, u1.data_ptr(),
-                                   u2.data_ptr(), tok.data_ptr(), acc.data_ptr(), rew.data_ptr(), adv.data_ptr(),
+                                   u2.data_ptr(), tok.data_ptr(), rew.data_ptr(), adv.data_ptr(),
                                    1e-6, 0, 0.0, ws.data_ptr(), ws.numel(), stream.cuda_stream)
         _lib.check(st, "aal_sim_accept_grpo")
-    return fn, stream
+    return fn, stream, {"token": tok, "reward": rew, "advantage": adv}
 
 
 def general_call(zd, zt, layout, B, S, K, weights, grad_dtype):
@@ -214,10 +286,10 @@ def general_call(zd, zt, layout, B, S, K, weights, grad_dtype):
                                 loss.data_ptr(), terms.data_ptr(), None, None, None, None, None, grad.data_ptr(),
                                 gcode, None, 0, ws.data_ptr(), ws.numel(), stream.cuda_stream)
         _lib.check(st, "aal_loss_fwd_bwd")
-    return fn, stream, R, W
+    return fn, stream, R, W, {"loss": loss, "terms": terms, "grad": grad}
 
 
-def vp_call(zd_s, zt_s, v0, R, N, K, mode, grad_dtype):
+def vp_call(zd_s, zt_s, v0, V, R, N, K, mode, grad_dtype):
     """A zero-allocation closure over one rank's five vocabulary-parallel calls
     on its [rows, V_slice] slice.  The rank's own records copied into every
     rank's place stand in for the two all-gathers' outputs."""
@@ -240,8 +312,8 @@ def vp_call(zd_s, zt_s, v0, R, N, K, mode, grad_dtype):
     s = stream.cuda_stream
 
     def fn():
-        _lib.check(L.aal_vp_row_partials(zd_s.data_ptr(), zt_s.data_ptr(), None, dcode, rows, vs, v0, mode, 1.0,
-                                         1.0, parts[0].data_ptr(), s), "aal_vp_row_partials")
+        _lib.check(L.aal_vp_row_partials(zd_s.data_ptr(), zt_s.data_ptr(), None, dcode, rows, vs, v0, V, mode,
+                                         1.0, 1.0, parts[0].data_ptr(), s), "aal_vp_row_partials")
         parts[1:].copy_(parts[0].expand(R - 1, -1, -1))
         _lib.check(L.aal_vp_merge_rows(parts.data_ptr(), R, rows, mode, 1.0, 1.0, row.data_ptr(), s),
                    "aal_vp_merge_rows")
@@ -253,7 +325,7 @@ def vp_call(zd_s, zt_s, v0, R, N, K, mode, grad_dtype):
                                         loss.data_ptr(), E.data_ptr(), None, None, s), "aal_vp_window_scan")
         _lib.check(L.aal_vp_grad(zd_s.data_ptr(), zt_s.data_ptr() if wtv else None, dcode, rows, vs, v0, mode,
                                  1.0, 1.0, row.data_ptr(), grad.data_ptr(), gcode, s), "aal_vp_grad")
-    return fn, stream
+    return fn, stream, {"loss": loss, "E": E, "grad": grad}
 
 
 def grpo_call(zth, zref, zt, m, K, grad_dtype):
@@ -283,7 +355,7 @@ def grpo_call(zth, zref, zt, m, K, grad_dtype):
                                 tt.data_ptr(), tr.data_ptr(), adv.data_ptr(), lrho.data_ptr(), grad.data_ptr(),
                                 gcode, None, ws.data_ptr(), ws.numel(), stream.cuda_stream)
         _lib.check(st, "aal_grpo_fwd_bwd")
-    return fn, stream
+    return fn, stream, {"loss": loss, "tau_theta": tt, "advantage": adv, "grad": grad}
 
 
 def _free_gpu(torch):
@@ -325,8 +397,10 @@ def main():
     s_in = 2 if cfg["dtype"] == torch.bfloat16 else 4
     gdt = cfg["dtype"]
     s_g = s_in
-    fn, stream, _ = loss_call("wtv", inp, gdt, args.flags)
+    fn, stream, outs = loss_call("wtv", inp, gdt, args.flags)
     ms = _time_calls(fn, args.steps, args.warmup, stream)
+    valid = check_outputs(fn, outs, "wtv", e_max=K)
+    del outs
     alg_bytes = rows * (2 * s_in + s_g) * V
     achieved = alg_bytes / (ms * 1e-3) / 1e9
     out = {
@@ -350,6 +424,8 @@ def main():
                      "kernel": "k_resident (timed: the whole aal_wtv_fwd_bwd call, i.e. k_resident plus "
                                "three microsecond-scale set-up/reduction kernels)"},
         "cpu_baseline": cpu,
+        "validation": valid,
+        "practical_ceilings": ceilings(dev),
     }
     if args.copy_calibration:
         src = torch.empty(1 << 32, dtype=torch.uint8, device=dev)
@@ -363,8 +439,10 @@ def main():
         torch.cuda.empty_cache()
     if not args.no_also:
         also = {}
-        fn_e, st_e, _ = loss_call("eal", inp, gdt, args.flags)
+        fn_e, st_e, o_e = loss_call("eal", inp, gdt, args.flags)
         ms_e = _time_calls(fn_e, args.steps, args.warmup, st_e)
+        check_outputs(fn_e, o_e, "eal", e_max=K)
+        del o_e
         also["eal_same_inputs"] = {"ms": ms_e, "rows_per_s": rows / (ms_e * 1e-3),
                                    "windows_per_s": N / (ms_e * 1e-3),
                                    "alg_GBps": rows * (2 * s_in + s_g) * V / (ms_e * 1e-3) / 1e9}
@@ -376,8 +454,10 @@ def main():
                     ("kl_plus_0.1eal_c2", _lib.AAL_LAYOUT_WINDOWS, N, K, (0.0, 0.1, 1.0, 0.0)),
                     ("kl_plus_tv_c2", _lib.AAL_LAYOUT_WINDOWS, N, K, (0.0, 0.0, 1.0, 1.0))]
             for name, layout, B_, S_, wts in legs:
-                fn_g, st_g, R_, W_ = general_call(zd, zt, layout, B_, S_, K, wts, gdt)
+                fn_g, st_g, R_, W_, o_g = general_call(zd, zt, layout, B_, S_, K, wts, gdt)
                 ms_g = _time_calls(fn_g, args.steps, args.warmup, st_g)
+                check_outputs(fn_g, o_g, name)
+                del fn_g, o_g
                 also[name] = {"ms": ms_g, "rows_per_s": R_ / (ms_g * 1e-3), "windows_per_s": W_ / (ms_g * 1e-3),
                               "alg_GBps": R_ * (2 * s_in + s_g) * V / (ms_g * 1e-3) / 1e9,
                               "entry": "aal_loss_fwd_bwd", "weights(wtv,eal,kl,tv)": wts}
@@ -387,8 +467,10 @@ def main():
             g_ = torch.Generator(device=dev).manual_seed(11)
             zref = (zd.float() + 0.5 * torch.randn(zd.shape, generator=g_, device=dev)).to(zd.dtype)
             shp = (N // m_, m_ * K, V)
-            fn_r, st_r = grpo_call(zd.view(shp), zref.view(shp), zt.view(shp), m_, K, gdt)
+            fn_r, st_r, o_r = grpo_call(zd.view(shp), zref.view(shp), zt.view(shp), m_, K, gdt)
             ms_r = _time_calls(fn_r, args.steps, args.warmup, st_r)
+            check_outputs(fn_r, o_r, "grpo")
+            del fn_r, o_r
             also["grpo_c2_m8"] = {"ms": ms_r, "rows_per_s": rows / (ms_r * 1e-3), "windows_per_s": N / (ms_r * 1e-3),
                                   "alg_GBps": rows * (3 * s_in + s_g) * V / (ms_r * 1e-3) / 1e9,
                                   "entry": "aal_grpo_fwd_bwd", "groups": N // m_, "m": m_}
@@ -399,8 +481,10 @@ def main():
             zd_s = zd.view(rows, V)[:, 3 * vs:4 * vs].contiguous()
             zt_s = zt.view(rows, V)[:, 3 * vs:4 * vs].contiguous()
             for name, mode in (("vp_wtv_c2_rank_share_8", _lib.AAL_VP_WTV), ("vp_eal_c2_rank_share_8", _lib.AAL_VP_EAL)):
-                fn_v, st_v = vp_call(zd_s, zt_s, 3 * vs, R_vp, N, K, mode, gdt)
+                fn_v, st_v, o_v = vp_call(zd_s, zt_s, 3 * vs, V, R_vp, N, K, mode, gdt)
                 ms_v = _time_calls(fn_v, args.steps, args.warmup, st_v)
+                check_outputs(fn_v, o_v, name, e_max=K)
+                del fn_v, o_v
                 also[name] = {"ms": ms_v, "rows_per_s": rows / (ms_v * 1e-3),
                               "alg_GBps": rows * (2 * s_in + s_g) * vs / (ms_v * 1e-3) / 1e9,
                               "entry": "aal_vp_*", "shape": f"{rows}x{vs} (V={V} over {R_vp} ranks)"}
@@ -411,23 +495,36 @@ def main():
         sim = make_config("c5", seed=0, device=dev)
         c5 = CONFIGS["c5"]
         rows5 = c5["P"] * c5["G"] * c5["K"]
-        fn_s, st_s = sim_call(sim)
+        fn_s, st_s, o_s = sim_call(sim)
         ms_s = _time_calls(fn_s, args.steps, args.warmup, st_s)
+        check_outputs(fn_s, o_s, "sim")
+        rw = o_s["reward"]
+        if rw.min().item() < 0 or rw.max().item() > c5["K"]:
+            _fail("sim: reward outside [0, K]")
+        del o_s
         also["sim_grpo_c5"] = {"ms": ms_s, "rows_per_s": rows5 / (ms_s * 1e-3),
                                "windows_per_s": c5["P"] * c5["G"] / (ms_s * 1e-3),
                                "alg_GBps": rows5 * 2 * 2 * c5["V"] / (ms_s * 1e-3) / 1e9}
         del fn_s, st_s
         if args.workload == "c2":
             # every other loss workload, each timed the same way (parity cases in the tests)
-            for name, op in (("c1_eal_fp32", "eal"), ("c3_eal_bf16", "eal"), ("c3_wtv_bf16_T0.7", "wtv"),
-                             ("c4_wtv_fp32_T0.5", "wtv")):
+            # (c3 EAL also at T_d = 0.7: the workload states no draft temperature
+            # for its greedy leg, so both readings are measured)
+            prev = None
+            for name, op, td_c in (("c1_eal_fp32", "eal", None), ("c3_eal_bf16", "eal", None),
+                                   ("c3_eal_bf16_Td0.7", "eal", 0.7), ("c3_wtv_bf16_T0.7", "wtv", None),
+                                   ("c4_wtv_fp32_T0.5", "wtv", None)):
                 wl = name[:2]
                 c = CONFIGS[wl]
-                del sim
-                _free_gpu(torch)
-                sim = make_config(wl, seed=0, device=dev)
-                fn_c, st_c, _ = loss_call(op, sim, c["dtype"], args.flags)
+                if wl != prev:
+                    del sim
+                    _free_gpu(torch)
+                    sim = make_config(wl, seed=0, device=dev)
+                    prev = wl
+                fn_c, st_c, o_c = loss_call(op, sim, c["dtype"], args.flags, temp_draft=td_c)
                 ms_c = _time_calls(fn_c, args.steps, args.warmup, st_c)
+                check_outputs(fn_c, o_c, name, e_max=c["K"])
+                del o_c
                 r_c = c["N"] * c["K"]
                 s_c = 2 if c["dtype"] == torch.bfloat16 else 4
                 gbps = r_c * 3 * s_c * c["V"] / (ms_c * 1e-3) / 1e9

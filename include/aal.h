@@ -23,9 +23,8 @@
  * Pointers.  Every array argument is a DEVICE pointer into memory the caller
  *   allocated and owns (e.g. a torch tensor).  The library never allocates,
  *   frees, or keeps a pointer past the call.
- * Streams.  `stream` is a hipStream_t passed as void* (NULL = the default
- *   stream).  Every call only enqueues kernels on it and returns; results are
- *   valid once the stream has been synchronised.  No call synchronises the
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Every
+ *   call only enqueues kernels on it and returns; results are valid once the stream has been synchronised.  No call synchronises the
  *   host.
  * Layout.  Logits are contiguous row-major [N, K, V] (simulation: [P, G, K, V]);
  *   row r = n*K + k holds position k of window n; the row stride is V elements.
@@ -54,6 +53,11 @@
 extern "C" {
 #endif
 
+/* HIP's stream handle, declared exactly as the HIP runtime declares it, so
+ * that this header stands alone (C11 / C++: repeating the typedef after
+ * <hip/hip_runtime.h> is allowed).  NULL is the default stream. */
+typedef struct ihipStream_t* hipStream_t;
+
 /* Element types of logits and gradients. */
 typedef enum { AAL_BF16 = 0, AAL_F32 = 1 } aal_dtype_t;
 
@@ -79,7 +83,7 @@ int aal_version(void);
 size_t aal_workspace_bytes(int64_t rows, int64_t windows);
 
 /* Static text for a status code ("unknown status" for others). */
-const char* aal_status_string(int status);
+const char* aal_status_string(aal_status_t status);
 
 /* Text describing the last error raised on the calling thread ("" if none).
  * The pointer stays valid until the thread's next library call. */
@@ -108,15 +112,31 @@ const char* aal_last_error(void);
  *                     AAL_BF16 (rounded to nearest even).
  * grad_scale        : device float scalar multiplying the gradient (an
  *                     upstream dL/dloss), or NULL for 1.0.  Not applied to loss.
- * flags             : AAL_FLAG_* bits.
+ * workspace         : at least aal_workspace_bytes(N*K, N) bytes, 256-byte aligned.
+ * The default schedule is one register-resident kernel when V is a multiple
+ * of 8 (bf16) / 4 (fp32) elements, K is in {1..8, 16} and a window fits the
+ * co-resident grid; every other shape takes the multi-kernel streaming
+ * schedule.  A poll time-out of the resident schedule (not expected) sets
+ * the loss to NaN.
  */
 aal_status_t aal_eal_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
                              int64_t N, int32_t K, int32_t V, float temp_draft,
                              float* loss, float* eal_per_window, float* accept,
                              int32_t* target_argmax,
                              void* grad_draft, aal_dtype_t grad_dtype, const float* grad_scale,
-                             uint32_t flags, void* workspace, size_t workspace_bytes,
-                             void* stream);
+                             void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* aal_eal_fwd_bwd with schedule flags: flags = 0 is aal_eal_fwd_bwd;
+ * AAL_FLAG_STREAMING forces the multi-kernel schedule (the same results
+ * within the stated tolerances; used to cross-check the two schedules).
+ * Unknown bits give AAL_ERR_ARG. */
+aal_status_t aal_eal_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
+                                int64_t N, int32_t K, int32_t V, float temp_draft,
+                                float* loss, float* eal_per_window, float* accept,
+                                int32_t* target_argmax,
+                                void* grad_draft, aal_dtype_t grad_dtype, const float* grad_scale,
+                                uint32_t flags, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
 /*
  * Window-TV loss, forward and backward (Eq. loss_tv, Eq. acc_sample).
@@ -136,8 +156,16 @@ aal_status_t aal_wtv_fwd_bwd(const void* z_draft, const void* z_target, aal_dtyp
                              float temp_draft, float temp_target,
                              float* loss, float* eal_per_window, float* accept,
                              void* grad_draft, aal_dtype_t grad_dtype, const float* grad_scale,
-                             uint32_t flags, void* workspace, size_t workspace_bytes,
-                             void* stream);
+                             void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* aal_wtv_fwd_bwd with schedule flags, as aal_eal_fwd_bwd_ex. */
+aal_status_t aal_wtv_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
+                                int64_t N, int32_t K, int32_t V,
+                                float temp_draft, float temp_target,
+                                float* loss, float* eal_per_window, float* accept,
+                                void* grad_draft, aal_dtype_t grad_dtype, const float* grad_scale,
+                                uint32_t flags, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
 /*
  * Simulated acceptance length and group-relative advantage (Section "GRPO
@@ -155,16 +183,27 @@ aal_status_t aal_wtv_fwd_bwd(const void* z_draft, const void* z_target, aal_dtyp
  *
  * z_draft, z_target : [P,G,K,V] of in_dtype.  u1, u2 : [P*G*K] float in [0,1).
  * P, G, K, V >= 1; G > std_ddof; V <= 2^21; temperature finite and > 0; eps >= 0.
- * draft_token, accept : [P*G*K] int32, or NULL.
+ * draft_token : [P*G*K] int32, or NULL.
  * reward    : [P*G] int32, required.   advantage : [P*G] float, required.
+ * workspace : at least aal_workspace_bytes(P*G*K, P*G) bytes, 256-byte aligned.
  */
 aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
                                  int32_t P, int32_t G, int32_t K, int32_t V, float temperature,
                                  const float* u1, const float* u2,
-                                 int32_t* draft_token, int32_t* accept,
-                                 int32_t* reward, float* advantage,
+                                 int32_t* draft_token, int32_t* reward, float* advantage,
                                  float eps, int32_t std_ddof, float adv_clip,
-                                 void* workspace, size_t workspace_bytes, void* stream);
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* aal_sim_accept_grpo that also returns the per-position verification
+ * outcome: accept [P*G*K] int32 (1 = the drafted token passes, 0 = it is
+ * rejected; positions after the first rejection are evaluated too), or NULL. */
+aal_status_t aal_sim_accept_grpo_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
+                                    int32_t P, int32_t G, int32_t K, int32_t V, float temperature,
+                                    const float* u1, const float* u2,
+                                    int32_t* draft_token, int32_t* accept,
+                                    int32_t* reward, float* advantage,
+                                    float eps, int32_t std_ddof, float adv_clip,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Row layouts of the combined-objective entry point. */
 typedef enum {
@@ -237,7 +276,7 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
                               float* e_tv, float* e_eal, float* accept_tv, float* accept_eal,
                               int32_t* xstar, void* grad_draft, aal_dtype_t grad_dtype,
                               const float* grad_scale, uint32_t flags, void* workspace,
-                              size_t workspace_bytes, void* stream);
+                              size_t workspace_bytes, hipStream_t stream);
 
 /* Constants of the GRPO loss that the paper leaves unstated (its Eq. advantage
  * uses eps = 1e-6). */
@@ -296,7 +335,7 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
                               float* loss, int32_t* tau_theta, int32_t* tau_ref, float* advantage,
                               float* log_rho, void* grad_theta, aal_dtype_t grad_dtype,
                               const float* grad_scale, void* workspace, size_t workspace_bytes,
-                              void* stream);
+                              hipStream_t stream);
 
 /*
  * Vocabulary-parallel pieces of aal_eal_fwd_bwd and aal_wtv_fwd_bwd: the work
@@ -364,19 +403,20 @@ typedef struct {
 
 /*
  * Step 1.  z_draft, z_target : [rows, V_slice] of in_dtype, the slice that
- * starts at global vocabulary index v0.  rows >= 1, V_slice >= 1, v0 >= 0,
- * v0 + V_slice < 2^31, rows*V_slice < 2^62.  EAL ignores temp_target.
+ * starts at global vocabulary index v0 of a vocabulary of V_total entries.
+ * rows >= 1, V_slice >= 1, v0 >= 0, v0 + V_slice <= V_total < 2^31,
+ * rows*V_slice < 2^62.  EAL ignores temp_target.
  * labels : EAL only, [rows] int32 global token ids that replace the target's
- *          greedy token (as in aal_loss_fwd_bwd), or NULL.  With labels the
- *          target logits are not read and z_target may be NULL; the slice
- *          that holds a row's label supplies its candidate, and a label that
- *          lies in no slice leaves the row without one (x* = 0, a = 0).
+ *          greedy token, or NULL.  As in aal_loss_fwd_bwd, an id outside
+ *          [0, V_total) is clamped into it.  With labels the target logits
+ *          are not read and z_target may be NULL; the slice that holds a
+ *          row's (clamped) label supplies its candidate.
  * parts : [rows] records, required.
  */
 aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, const int32_t* labels,
                                  aal_dtype_t in_dtype, int64_t rows, int32_t V_slice, int32_t v0,
-                                 aal_vp_mode_t mode, float temp_draft, float temp_target,
-                                 aal_vp_part_t* parts, void* stream);
+                                 int32_t V_total, aal_vp_mode_t mode, float temp_draft,
+                                 float temp_target, aal_vp_part_t* parts, hipStream_t stream);
 
 /*
  * Step 2.  parts_all : [R, rows] records, rank-major (rank r's records at
@@ -387,14 +427,14 @@ aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, cons
  */
 aal_status_t aal_vp_merge_rows(const aal_vp_part_t* parts_all, int32_t R, int64_t rows,
                                aal_vp_mode_t mode, float temp_draft, float temp_target,
-                               aal_vp_row_t* row, void* stream);
+                               aal_vp_row_t* row, hipStream_t stream);
 
 /*
  * Step 3 (WTV).  The slice as in step 1, row from step 2.  acc : [rows], required.
  */
 aal_status_t aal_vp_accept_partials(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
                                     int64_t rows, int32_t V_slice, float temp_draft, float temp_target,
-                                    const aal_vp_row_t* row, aal_vp_acc_t* acc, void* stream);
+                                    const aal_vp_row_t* row, aal_vp_acc_t* acc, hipStream_t stream);
 
 /*
  * Step 4.  row : [N*K] records from step 2, updated in place (WTV: a and qlt
@@ -407,7 +447,7 @@ aal_status_t aal_vp_accept_partials(const void* z_draft, const void* z_target, a
 aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R,
                                 int64_t N, int32_t K, aal_vp_mode_t mode, float temp_draft,
                                 const float* grad_scale, float* loss, float* eal_per_window,
-                                float* accept, int32_t* target_argmax, void* stream);
+                                float* accept, int32_t* target_argmax, hipStream_t stream);
 
 /*
  * Step 4 for sequences (the layout of aal_loss_fwd_bwd with
@@ -426,7 +466,7 @@ aal_status_t aal_vp_sequence_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all
                                   int64_t B, int32_t S, int32_t K, aal_vp_mode_t mode,
                                   float temp_draft, const float* grad_scale, float* loss,
                                   float* eal_per_window, float* accept, int32_t* target_argmax,
-                                  void* stream);
+                                  hipStream_t stream);
 
 /*
  * Step 5.  The slice as in step 1 (EAL reads only z_draft; z_target may then be
@@ -436,7 +476,7 @@ aal_status_t aal_vp_sequence_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all
 aal_status_t aal_vp_grad(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
                          int64_t rows, int32_t V_slice, int32_t v0, aal_vp_mode_t mode,
                          float temp_draft, float temp_target, const aal_vp_row_t* row,
-                         void* grad_draft, aal_dtype_t grad_dtype, void* stream);
+                         void* grad_draft, aal_dtype_t grad_dtype, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -55,7 +55,6 @@ __all__ = [
     "group_advantage",
     "sim_accept_grpo",
     "sim_near_threshold",
-    "wtv_near_ties",
     "LAYOUT_WINDOWS",
     "LAYOUT_SEQUENCES",
     "window_rows",
@@ -549,12 +548,3 @@ def sim_near_threshold(z_draft, z_target, T: float, u1, u2, tol: float = 1e-6):
     near2 = np.abs(np.asarray(u2, np.float64) - thr) <= tol
     return near1 | near2
 
-
-def wtv_near_ties(z_draft, z_target, T_draft: float, T_target: float, rel: float = 1e-5):
-    """Per row: the largest q(v) among entries whose q and p agree to ``rel``
-    relative.  At such entries 1[q < p] may flip between precisions; the
-    gradient of the row then moves by at most |coef| * q(v) * (1 + max q)."""
-    q = np.exp(tempered_log_softmax(z_draft, T_draft))
-    p = np.exp(tempered_log_softmax(z_target, T_target))
-    near = np.abs(q - p) <= rel * np.maximum(p, q)
-    return np.max(np.where(near, q, 0.0), axis=-1)

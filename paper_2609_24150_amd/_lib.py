@@ -50,13 +50,28 @@ _SIGNATURES = {
         _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_float,
         _vp, _vp, _vp, _vp,
         _vp, C.c_int, _vp,
+        _vp, C.c_size_t, _vp]),
+    "aal_eal_fwd_bwd_ex": (C.c_int, [
+        _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_float,
+        _vp, _vp, _vp, _vp,
+        _vp, C.c_int, _vp,
         C.c_uint32, _vp, C.c_size_t, _vp]),
     "aal_wtv_fwd_bwd": (C.c_int, [
         _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_float, C.c_float,
         _vp, _vp, _vp,
         _vp, C.c_int, _vp,
+        _vp, C.c_size_t, _vp]),
+    "aal_wtv_fwd_bwd_ex": (C.c_int, [
+        _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_float, C.c_float,
+        _vp, _vp, _vp,
+        _vp, C.c_int, _vp,
         C.c_uint32, _vp, C.c_size_t, _vp]),
     "aal_sim_accept_grpo": (C.c_int, [
+        _vp, _vp, C.c_int, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_float,
+        _vp, _vp, _vp, _vp, _vp,
+        C.c_float, C.c_int32, C.c_float,
+        _vp, C.c_size_t, _vp]),
+    "aal_sim_accept_grpo_ex": (C.c_int, [
         _vp, _vp, C.c_int, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_float,
         _vp, _vp, _vp, _vp, _vp, _vp,
         C.c_float, C.c_int32, C.c_float,
@@ -72,7 +87,8 @@ _SIGNATURES = {
         C.c_int32, _vp, C.c_float, GrpoParams, _vp, _vp, _vp, _vp, _vp,
         _vp, C.c_int, _vp, _vp, C.c_size_t, _vp]),
     "aal_vp_row_partials": (C.c_int, [
-        _vp, _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_float, C.c_float, _vp, _vp]),
+        _vp, _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int, C.c_float, C.c_float, _vp,
+        _vp]),
     "aal_vp_merge_rows": (C.c_int, [_vp, C.c_int32, C.c_int64, C.c_int, C.c_float, C.c_float, _vp, _vp]),
     "aal_vp_accept_partials": (C.c_int, [
         _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_float, C.c_float, _vp, _vp, _vp]),

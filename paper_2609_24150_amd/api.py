@@ -79,11 +79,14 @@ def aal_eal_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor, temp_draft: f
         ws = workspace(N * K, N, dev)
     if grad_scale is not None and (grad_scale.dtype != torch.float32 or grad_scale.device != dev):
         raise TypeError("grad_scale must be a float32 device tensor")
-    st = _lib.lib().aal_eal_fwd_bwd(
-        _ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), N, K, V, float(temp_draft),
-        _ptr(out["loss"]), _ptr(out["E"]), _ptr(out["accept"]), _ptr(out["xstar"]),
-        _ptr(g), _dtype_code(g.dtype) if g is not None else AAL_F32, _ptr(grad_scale),
-        int(flags), _ptr(ws), ws.numel(), _stream(dev, stream))
+    args = [_ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), N, K, V, float(temp_draft),
+            _ptr(out["loss"]), _ptr(out["E"]), _ptr(out["accept"]), _ptr(out["xstar"]),
+            _ptr(g), _dtype_code(g.dtype) if g is not None else AAL_F32, _ptr(grad_scale)]
+    tail = [_ptr(ws), ws.numel(), _stream(dev, stream)]
+    if flags:
+        st = _lib.lib().aal_eal_fwd_bwd_ex(*args, int(flags), *tail)
+    else:
+        st = _lib.lib().aal_eal_fwd_bwd(*args, *tail)
     _lib.check(st, "aal_eal_fwd_bwd")
     return out
 
@@ -105,23 +108,28 @@ def aal_wtv_fwd_bwd(z_draft: torch.Tensor, z_target: torch.Tensor, temp_draft: f
         ws = workspace(N * K, N, dev)
     if grad_scale is not None and (grad_scale.dtype != torch.float32 or grad_scale.device != dev):
         raise TypeError("grad_scale must be a float32 device tensor")
-    st = _lib.lib().aal_wtv_fwd_bwd(
-        _ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), N, K, V,
-        float(temp_draft), float(temp_target),
-        _ptr(out["loss"]), _ptr(out["E"]), _ptr(out["accept"]),
-        _ptr(g), _dtype_code(g.dtype) if g is not None else AAL_F32, _ptr(grad_scale),
-        int(flags), _ptr(ws), ws.numel(), _stream(dev, stream))
+    args = [_ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), N, K, V,
+            float(temp_draft), float(temp_target),
+            _ptr(out["loss"]), _ptr(out["E"]), _ptr(out["accept"]),
+            _ptr(g), _dtype_code(g.dtype) if g is not None else AAL_F32, _ptr(grad_scale)]
+    tail = [_ptr(ws), ws.numel(), _stream(dev, stream)]
+    if flags:
+        st = _lib.lib().aal_wtv_fwd_bwd_ex(*args, int(flags), *tail)
+    else:
+        st = _lib.lib().aal_wtv_fwd_bwd(*args, *tail)
     _lib.check(st, "aal_wtv_fwd_bwd")
     return out
 
 
 def aal_sim_accept_grpo(z_draft: torch.Tensor, z_target: torch.Tensor, u1: torch.Tensor, u2: torch.Tensor,
                         temperature: float = 1.0, *, eps: float = 1e-6, std_ddof: int = 0,
-                        adv_clip: float = 0.0, ws: torch.Tensor | None = None, stream=None) -> dict:
+                        adv_clip: float = 0.0, accept: bool = True, ws: torch.Tensor | None = None,
+                        stream=None) -> dict:
     """Simulated acceptance length and group advantages on [P, G, K, V] logits
     with uniforms u1, u2 of shape [P, G, K].
 
-    Returns a dict: token [P, G, K] int32, accept [P, G, K] int32,
+    Returns a dict: token [P, G, K] int32, accept [P, G, K] int32 (None with
+    accept=False, which calls the entry point without that output),
     reward [P, G] int32, advantage [P, G] float32."""
     _check_logits(z_draft, z_target, 4)
     P, G, K, V = z_draft.shape
@@ -131,17 +139,20 @@ def aal_sim_accept_grpo(z_draft: torch.Tensor, z_target: torch.Tensor, u1: torch
             raise ValueError("u1 and u2 must be contiguous float32 device tensors of shape [P, G, K]")
     out = {
         "token": torch.empty(P, G, K, dtype=torch.int32, device=dev),
-        "accept": torch.empty(P, G, K, dtype=torch.int32, device=dev),
+        "accept": torch.empty(P, G, K, dtype=torch.int32, device=dev) if accept else None,
         "reward": torch.empty(P, G, dtype=torch.int32, device=dev),
         "advantage": torch.empty(P, G, dtype=torch.float32, device=dev),
     }
     if ws is None:
         ws = workspace(P * G * K, P * G, dev)
-    st = _lib.lib().aal_sim_accept_grpo(
-        _ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), P, G, K, V, float(temperature),
-        _ptr(u1), _ptr(u2), _ptr(out["token"]), _ptr(out["accept"]), _ptr(out["reward"]),
-        _ptr(out["advantage"]), float(eps), int(std_ddof), float(adv_clip),
-        _ptr(ws), ws.numel(), _stream(dev, stream))
+    head = [_ptr(z_draft), _ptr(z_target), _dtype_code(z_draft.dtype), P, G, K, V, float(temperature),
+            _ptr(u1), _ptr(u2), _ptr(out["token"])]
+    tail = [_ptr(out["reward"]), _ptr(out["advantage"]), float(eps), int(std_ddof), float(adv_clip),
+            _ptr(ws), ws.numel(), _stream(dev, stream)]
+    if accept:
+        st = _lib.lib().aal_sim_accept_grpo_ex(*head, _ptr(out["accept"]), *tail)
+    else:
+        st = _lib.lib().aal_sim_accept_grpo(*head, *tail)
     _lib.check(st, "aal_sim_accept_grpo")
     return out
 
@@ -288,10 +299,11 @@ def _records(t: torch.Tensor, nbytes: int, name: str, lead: int):
 
 
 def aal_vp_row_partials(z_draft: torch.Tensor, z_target: torch.Tensor | None, v0: int, mode: int,
-                        temp_draft: float = 1.0, temp_target: float = 1.0, *, labels: torch.Tensor | None = None,
-                        stream=None) -> torch.Tensor:
-    """Step 1: partial row statistics of the slice [v0, v0 + V_slice).  EAL may
-    take int32 labels [rows] (global token ids) in place of the target's greedy
+                        temp_draft: float = 1.0, temp_target: float = 1.0, *, V_total: int,
+                        labels: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Step 1: partial row statistics of the slice [v0, v0 + V_slice) of a
+    vocabulary of V_total entries.  EAL may take int32 labels [rows] (global
+    token ids, clamped into [0, V_total)) in place of the target's greedy
     token; the target slice may then be None.  Returns [rows, 32] records."""
     rows, vs, dev = _vp_slice(z_draft, z_target, need_target=labels is None)
     if labels is not None and (labels.dtype != torch.int32 or labels.numel() != rows or labels.device != dev
@@ -299,7 +311,8 @@ def aal_vp_row_partials(z_draft: torch.Tensor, z_target: torch.Tensor | None, v0
         raise ValueError("labels must be a contiguous int32 device tensor with one entry per row")
     parts = torch.empty(rows, _lib.VP_PART_BYTES, dtype=torch.uint8, device=dev)
     st = _lib.lib().aal_vp_row_partials(_ptr(z_draft), _ptr(z_target), _ptr(labels), _dtype_code(z_draft.dtype),
-                                        rows, vs, int(v0), int(mode), float(temp_draft), float(temp_target),
+                                        rows, vs, int(v0), int(V_total), int(mode), float(temp_draft),
+                                        float(temp_target),
                                         _ptr(parts), _stream(dev, stream))
     _lib.check(st, "aal_vp_row_partials")
     return parts

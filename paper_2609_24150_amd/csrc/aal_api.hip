@@ -8,19 +8,19 @@
 #include <stdio.h>
 #include <string.h>
 
-#include <string>
-
 namespace {
 
-thread_local std::string g_last_error;
+// A plain per-thread buffer: nothing to construct or destroy at thread or
+// process exit.
+thread_local char g_last_error[512];
+
+void clear_error() { g_last_error[0] = '\0'; }
 
 aal_status_t fail(aal_status_t s, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return s;
 }
 
@@ -135,8 +135,8 @@ size_t aal_workspace_bytes(int64_t rows, int64_t windows) {
   return aal::workspace_bytes(rows, windows);
 }
 
-const char* aal_status_string(int status) {
-  switch (status) {
+const char* aal_status_string(aal_status_t status) {
+  switch (int(status)) {
     case AAL_OK: return "AAL_OK";
     case AAL_ERR_ARG: return "AAL_ERR_ARG: invalid argument";
     case AAL_ERR_DTYPE: return "AAL_ERR_DTYPE: unsupported element type";
@@ -147,14 +147,14 @@ const char* aal_status_string(int status) {
   }
 }
 
-const char* aal_last_error(void) { return g_last_error.c_str(); }
+const char* aal_last_error(void) { return g_last_error; }
 
-aal_status_t aal_eal_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N, int32_t K,
-                             int32_t V, float temp_draft, float* loss, float* eal_per_window, float* accept,
-                             int32_t* target_argmax, void* grad_draft, aal_dtype_t grad_dtype,
-                             const float* grad_scale, uint32_t flags, void* workspace, size_t workspace_bytes,
-                             void* stream) {
-  g_last_error.clear();
+aal_status_t aal_eal_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N,
+                                int32_t K, int32_t V, float temp_draft, float* loss, float* eal_per_window,
+                                float* accept, int32_t* target_argmax, void* grad_draft, aal_dtype_t grad_dtype,
+                                const float* grad_scale, uint32_t flags, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  clear_error();
   const CommonIn c{z_draft, z_target, int(in_dtype), N, K, V, loss, grad_draft, int(grad_dtype),
                    workspace, workspace_bytes};
   aal_status_t s = validate_common(c);
@@ -182,15 +182,16 @@ aal_status_t aal_eal_fwd_bwd(const void* z_draft, const void* z_target, aal_dtyp
   a.xstar = target_argmax;
   a.grad = grad_draft;
   a.grad_scale = grad_scale;
-  a.stream = static_cast<hipStream_t>(stream);
+  a.stream = stream;
   return run_loss(a, flags);
 }
 
-aal_status_t aal_wtv_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N, int32_t K,
-                             int32_t V, float temp_draft, float temp_target, float* loss, float* eal_per_window,
-                             float* accept, void* grad_draft, aal_dtype_t grad_dtype, const float* grad_scale,
-                             uint32_t flags, void* workspace, size_t workspace_bytes, void* stream) {
-  g_last_error.clear();
+aal_status_t aal_wtv_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N,
+                                int32_t K, int32_t V, float temp_draft, float temp_target, float* loss,
+                                float* eal_per_window, float* accept, void* grad_draft, aal_dtype_t grad_dtype,
+                                const float* grad_scale, uint32_t flags, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  clear_error();
   const CommonIn c{z_draft, z_target, int(in_dtype), N, K, V, loss, grad_draft, int(grad_dtype),
                    workspace, workspace_bytes};
   aal_status_t s = validate_common(c);
@@ -221,16 +222,16 @@ aal_status_t aal_wtv_fwd_bwd(const void* z_draft, const void* z_target, aal_dtyp
   a.xstar = nullptr;
   a.grad = grad_draft;
   a.grad_scale = grad_scale;
-  a.stream = static_cast<hipStream_t>(stream);
+  a.stream = stream;
   return run_loss(a, flags);
 }
 
-aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int32_t P,
-                                 int32_t G, int32_t K, int32_t V, float temperature, const float* u1,
-                                 const float* u2, int32_t* draft_token, int32_t* accept, int32_t* reward,
-                                 float* advantage, float eps, int32_t std_ddof, float adv_clip, void* workspace,
-                                 size_t workspace_bytes, void* stream) {
-  g_last_error.clear();
+aal_status_t aal_sim_accept_grpo_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int32_t P,
+                                    int32_t G, int32_t K, int32_t V, float temperature, const float* u1,
+                                    const float* u2, int32_t* draft_token, int32_t* accept, int32_t* reward,
+                                    float* advantage, float eps, int32_t std_ddof, float adv_clip, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream) {
+  clear_error();
   if (!z_draft || !z_target || !u1 || !u2) return fail(AAL_ERR_ARG, "z_draft, z_target, u1, u2 must be non-NULL");
   if (!reward || !advantage) return fail(AAL_ERR_ARG, "reward and advantage must be non-NULL");
   if (P < 1 || G < 1 || K < 1 || V < 1) return fail(AAL_ERR_ARG, "P, G, K, V must be >= 1");
@@ -270,10 +271,35 @@ aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_
   a.eps = eps;
   a.ddof = std_ddof;
   a.clip = adv_clip;
-  a.stream = static_cast<hipStream_t>(stream);
+  a.stream = stream;
   hipError_t e = aal::launch_sim(a);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
+}
+
+aal_status_t aal_eal_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N, int32_t K,
+                             int32_t V, float temp_draft, float* loss, float* eal_per_window, float* accept,
+                             int32_t* target_argmax, void* grad_draft, aal_dtype_t grad_dtype,
+                             const float* grad_scale, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return aal_eal_fwd_bwd_ex(z_draft, z_target, in_dtype, N, K, V, temp_draft, loss, eal_per_window, accept,
+                            target_argmax, grad_draft, grad_dtype, grad_scale, 0u, workspace, workspace_bytes, stream);
+}
+
+aal_status_t aal_wtv_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N, int32_t K,
+                             int32_t V, float temp_draft, float temp_target, float* loss, float* eal_per_window,
+                             float* accept, void* grad_draft, aal_dtype_t grad_dtype, const float* grad_scale,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return aal_wtv_fwd_bwd_ex(z_draft, z_target, in_dtype, N, K, V, temp_draft, temp_target, loss, eal_per_window,
+                            accept, grad_draft, grad_dtype, grad_scale, 0u, workspace, workspace_bytes, stream);
+}
+
+aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int32_t P,
+                                 int32_t G, int32_t K, int32_t V, float temperature, const float* u1,
+                                 const float* u2, int32_t* draft_token, int32_t* reward, float* advantage, float eps,
+                                 int32_t std_ddof, float adv_clip, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
+  return aal_sim_accept_grpo_ex(z_draft, z_target, in_dtype, P, G, K, V, temperature, u1, u2, draft_token, nullptr,
+                                reward, advantage, eps, std_ddof, adv_clip, workspace, workspace_bytes, stream);
 }
 
 size_t aal_loss_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32_t K) {
@@ -289,8 +315,8 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
                               float temp_target, aal_loss_weights_t weights, float* loss, float* terms, float* e_tv,
                               float* e_eal, float* accept_tv, float* accept_eal, int32_t* xstar, void* grad_draft,
                               aal_dtype_t grad_dtype, const float* grad_scale, uint32_t flags, void* workspace,
-                              size_t workspace_bytes, void* stream) {
-  g_last_error.clear();
+                              size_t workspace_bytes, hipStream_t stream) {
+  clear_error();
   if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES)
     return fail(AAL_ERR_ARG, "unknown layout %d", int(layout));
   if (B < 1) return fail(AAL_ERR_ARG, "B must be >= 1 (got %lld)", (long long)B);
@@ -377,7 +403,7 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
   wp += 256;
   a.loss_parts = reinterpret_cast<double*>(wp);
   a.streaming = (flags & AAL_FLAG_STREAMING) != 0;
-  a.stream = static_cast<hipStream_t>(stream);
+  a.stream = stream;
   hipError_t e = aal::launch_general(a);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
@@ -397,8 +423,8 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
                               int32_t K, int32_t V, const int32_t* anchors, float temperature,
                               aal_grpo_params_t params, float* loss, int32_t* tau_theta, int32_t* tau_ref,
                               float* advantage, float* log_rho, void* grad_theta, aal_dtype_t grad_dtype,
-                              const float* grad_scale, void* workspace, size_t workspace_bytes, void* stream) {
-  g_last_error.clear();
+                              const float* grad_scale, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  clear_error();
   if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES)
     return fail(AAL_ERR_ARG, "unknown layout %d", int(layout));
   if (B < 1) return fail(AAL_ERR_ARG, "B must be >= 1 (got %lld)", (long long)B);
@@ -487,7 +513,7 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
   a.win_coef = reinterpret_cast<float*>(wp);
   wp += aal::align256(size_t(groups * m) * sizeof(float));
   a.group_loss = reinterpret_cast<float*>(wp);
-  a.stream = static_cast<hipStream_t>(stream);
+  a.stream = stream;
   hipError_t e = aal::launch_grpo(a);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
@@ -495,16 +521,19 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
 
 
 aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, const int32_t* labels,
-                                 aal_dtype_t in_dtype, int64_t rows, int32_t V_slice, int32_t v0,
+                                 aal_dtype_t in_dtype, int64_t rows, int32_t V_slice, int32_t v0, int32_t V_total,
                                  aal_vp_mode_t mode, float temp_draft, float temp_target, aal_vp_part_t* parts,
-                                 void* stream) {
-  g_last_error.clear();
+                                 hipStream_t stream) {
+  clear_error();
   if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
   if (labels && mode != AAL_VP_EAL) return fail(AAL_ERR_ARG, "labels are for EAL mode only");
   if (labels && !aligned(labels, 4)) return fail(AAL_ERR_ALIGN, "labels must be 4-byte aligned");
   aal_status_t st = validate_vp_slice(z_draft, labels ? nullptr : z_target, !labels, int(in_dtype), rows, V_slice,
                                       v0);
   if (st != AAL_OK) return st;
+  if (V_total < 1 || int64_t(v0) + V_slice > V_total)
+    return fail(AAL_ERR_ARG, "V_total must hold the slice: v0 + V_slice <= V_total (got %d + %d > %d)", v0, V_slice,
+                V_total);
   if (!parts) return fail(AAL_ERR_ARG, "parts must be non-NULL");
   if (!aligned(parts, 4)) return fail(AAL_ERR_ALIGN, "parts must be 4-byte aligned");
   aal::VpSlice s{};
@@ -516,16 +545,17 @@ aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, cons
   s.rows = rows;
   s.vs = V_slice;
   s.v0 = v0;
+  s.vtot = V_total;
   s.mode = vp_mode(int(mode));
-  s.stream = static_cast<hipStream_t>(stream);
+  s.stream = stream;
   const hipError_t e = aal::launch_vp_partials(s, parts);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
 }
 
 aal_status_t aal_vp_merge_rows(const aal_vp_part_t* parts_all, int32_t R, int64_t rows, aal_vp_mode_t mode,
-                               float temp_draft, float temp_target, aal_vp_row_t* row, void* stream) {
-  g_last_error.clear();
+                               float temp_draft, float temp_target, aal_vp_row_t* row, hipStream_t stream) {
+  clear_error();
   if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
   if (!parts_all || !row) return fail(AAL_ERR_ARG, "parts_all and row must be non-NULL");
   if (R < 1) return fail(AAL_ERR_ARG, "R must be >= 1 (got %d)", R);
@@ -536,15 +566,15 @@ aal_status_t aal_vp_merge_rows(const aal_vp_part_t* parts_all, int32_t R, int64_
   aal_status_t st = vp_scales(int(mode), temp_draft, temp_target, &scd, &sct);
   if (st != AAL_OK) return st;
   const hipError_t e =
-      aal::launch_vp_merge(parts_all, R, rows, vp_mode(int(mode)), scd, sct, row, static_cast<hipStream_t>(stream));
+      aal::launch_vp_merge(parts_all, R, rows, vp_mode(int(mode)), scd, sct, row, stream);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
 }
 
 aal_status_t aal_vp_accept_partials(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t rows,
                                     int32_t V_slice, float temp_draft, float temp_target, const aal_vp_row_t* row,
-                                    aal_vp_acc_t* acc, void* stream) {
-  g_last_error.clear();
+                                    aal_vp_acc_t* acc, hipStream_t stream) {
+  clear_error();
   aal_status_t st = validate_vp_slice(z_draft, z_target, true, int(in_dtype), rows, V_slice, 0);
   if (st != AAL_OK) return st;
   if (!row || !acc) return fail(AAL_ERR_ARG, "row and acc must be non-NULL");
@@ -558,7 +588,7 @@ aal_status_t aal_vp_accept_partials(const void* z_draft, const void* z_target, a
   s.vs = V_slice;
   s.v0 = 0;
   s.mode = aal::Mode::kWtv;
-  s.stream = static_cast<hipStream_t>(stream);
+  s.stream = stream;
   const hipError_t e = aal::launch_vp_accept(s, row, acc);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
@@ -566,8 +596,8 @@ aal_status_t aal_vp_accept_partials(const void* z_draft, const void* z_target, a
 
 aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R, int64_t N, int32_t K,
                                 aal_vp_mode_t mode, float temp_draft, const float* grad_scale, float* loss,
-                                float* eal_per_window, float* accept, int32_t* target_argmax, void* stream) {
-  g_last_error.clear();
+                                float* eal_per_window, float* accept, int32_t* target_argmax, hipStream_t stream) {
+  clear_error();
   if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
   if (!row || !loss || !eal_per_window) return fail(AAL_ERR_ARG, "row, loss and eal_per_window must be non-NULL");
   if (N < 1) return fail(AAL_ERR_ARG, "N must be >= 1 (got %lld)", (long long)N);
@@ -583,7 +613,7 @@ aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, 
   if (st != AAL_OK) return st;
   const hipError_t e = aal::launch_vp_scan(row, wtv ? acc_all : nullptr, wtv ? R : 0, N, K, vp_mode(int(mode)),
                                            1.0f / temp_draft, grad_scale, loss, eal_per_window, accept,
-                                           wtv ? nullptr : target_argmax, static_cast<hipStream_t>(stream));
+                                           wtv ? nullptr : target_argmax, stream);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
 }
@@ -591,8 +621,8 @@ aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, 
 aal_status_t aal_vp_sequence_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, int32_t R, int64_t B, int32_t S,
                                   int32_t K, aal_vp_mode_t mode, float temp_draft, const float* grad_scale,
                                   float* loss, float* eal_per_window, float* accept, int32_t* target_argmax,
-                                  void* stream) {
-  g_last_error.clear();
+                                  hipStream_t stream) {
+  clear_error();
   if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
   if (!row || !loss || !eal_per_window) return fail(AAL_ERR_ARG, "row, loss and eal_per_window must be non-NULL");
   if (B < 1) return fail(AAL_ERR_ARG, "B must be >= 1 (got %lld)", (long long)B);
@@ -610,15 +640,15 @@ aal_status_t aal_vp_sequence_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all
   const hipError_t e = aal::launch_vp_seq_scan(row, wtv ? acc_all : nullptr, wtv ? R : 0, B, S, K,
                                                vp_mode(int(mode)), 1.0f / temp_draft, grad_scale, loss,
                                                eal_per_window, accept, wtv ? nullptr : target_argmax,
-                                               static_cast<hipStream_t>(stream));
+                                               stream);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
 }
 
 aal_status_t aal_vp_grad(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t rows,
                          int32_t V_slice, int32_t v0, aal_vp_mode_t mode, float temp_draft, float temp_target,
-                         const aal_vp_row_t* row, void* grad_draft, aal_dtype_t grad_dtype, void* stream) {
-  g_last_error.clear();
+                         const aal_vp_row_t* row, void* grad_draft, aal_dtype_t grad_dtype, hipStream_t stream) {
+  clear_error();
   if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
   aal_status_t st =
       validate_vp_slice(z_draft, z_target, mode == AAL_VP_WTV, int(in_dtype), rows, V_slice, v0);
@@ -636,7 +666,7 @@ aal_status_t aal_vp_grad(const void* z_draft, const void* z_target, aal_dtype_t 
   s.vs = V_slice;
   s.v0 = v0;
   s.mode = vp_mode(int(mode));
-  s.stream = static_cast<hipStream_t>(stream);
+  s.stream = stream;
   const hipError_t e = aal::launch_vp_grad(s, row, grad_draft, to_dtype(grad_dtype));
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;

@@ -7,8 +7,7 @@
 
 #include <limits.h>
 
-#include <mutex>
-#include <vector>
+#include <atomic>
 
 namespace aal {
 namespace {
@@ -168,20 +167,28 @@ struct DevInfo {
   bool coop = false;
 };
 
+// Per-device attributes, cached in a fixed table of atomics: nothing here has
+// a destructor to run at process exit.  A device beyond the table is queried
+// on every call.
+constexpr int kMaxCachedDevices = 64;
+std::atomic<int> g_dev_cus[kMaxCachedDevices];   // 0 = not yet queried
+std::atomic<int> g_dev_coop[kMaxCachedDevices];
+
 DevInfo device_info() {
-  static std::mutex mu;
-  static std::vector<DevInfo> cache;
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return {};
-  std::lock_guard<std::mutex> lk(mu);
-  if (int(cache.size()) <= dev) cache.resize(dev + 1);
-  if (cache[dev].cus == 0) {
-    int cus = 0, coop = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return {};
-    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess) return {};
-    cache[dev] = {cus, coop != 0};
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return {};
+  if (dev < kMaxCachedDevices) {
+    const int cus = g_dev_cus[dev].load(std::memory_order_acquire);
+    if (cus != 0) return {cus, g_dev_coop[dev].load(std::memory_order_relaxed) != 0};
   }
-  return cache[dev];
+  int cus = 0, coop = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return {};
+  if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess) return {};
+  if (dev < kMaxCachedDevices) {
+    g_dev_coop[dev].store(coop, std::memory_order_relaxed);
+    g_dev_cus[dev].store(cus, std::memory_order_release);
+  }
+  return {cus, coop != 0};
 }
 
 }  // namespace

@@ -16,6 +16,7 @@ struct VpSlice {
   int64_t rows;
   int32_t vs;    // V_slice
   int32_t v0;    // global index of the slice's first entry
+  int32_t vtot;  // the whole vocabulary (labels are clamped into [0, vtot))
   Mode mode;
   float scd, sct;  // log2(e)/T of draft and target
   hipStream_t stream;

@@ -42,7 +42,7 @@ unsigned row_grid(int64_t rows) { return unsigned(rows < kMaxRowBlocks ? rows : 
 template <class TI, int MODE, bool VEC, int U, bool LAB>
 __global__ __launch_bounds__(kBlock) void k_vp_partials(const void* __restrict__ zd, const void* __restrict__ zt,
                                                         const int32_t* __restrict__ labels, int64_t rows, int Vs,
-                                                        int v0, float scd, float sct,
+                                                        int v0, int vtot, float scd, float sct,
                                                         aal_vp_part_t* __restrict__ parts) {
   using Gr = Groups<TI, VEC>;
   constexpr int E = Gr::E;
@@ -114,7 +114,9 @@ __global__ __launch_bounds__(kBlock) void k_vp_partials(const void* __restrict__
     out.reserved0 = 0;
     out.reserved1 = 0;
     if constexpr (LAB) {
-      const int64_t xl = int64_t(labels[row]) - v0;  // the label in slice coordinates
+      // the label clamped into the vocabulary [0, vtot), as the fused calls
+      // clamp it, then in slice coordinates
+      const int64_t xl = int64_t(min(max(labels[row], 0), vtot - 1)) - v0;
       if (xl >= 0 && xl < Vs) {
         out.zmax_t = 0.f;  // the only candidate of the row: its value decides nothing
         out.zd_at = TI::load1(zd, row * int64_t(Vs) + xl);
@@ -412,10 +414,10 @@ template <class TI, int MODE, bool LAB>
 void partials_lab(const VpSlice& s, aal_vp_part_t* parts) {
   const unsigned grid = row_grid(s.rows);
   if (s.vs % TI::kVec == 0)
-    k_vp_partials<TI, MODE, true, 4, LAB><<<grid, kBlock, 0, s.stream>>>(s.zd, s.zt, s.labels, s.rows, s.vs, s.v0,
+    k_vp_partials<TI, MODE, true, 4, LAB><<<grid, kBlock, 0, s.stream>>>(s.zd, s.zt, s.labels, s.rows, s.vs, s.v0, s.vtot,
                                                                           s.scd, s.sct, parts);
   else
-    k_vp_partials<TI, MODE, false, 8, LAB><<<grid, kBlock, 0, s.stream>>>(s.zd, s.zt, s.labels, s.rows, s.vs, s.v0,
+    k_vp_partials<TI, MODE, false, 8, LAB><<<grid, kBlock, 0, s.stream>>>(s.zd, s.zt, s.labels, s.rows, s.vs, s.v0, s.vtot,
                                                                            s.scd, s.sct, parts);
 }
 

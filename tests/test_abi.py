@@ -30,8 +30,53 @@ def test_header_declares_the_boundary():
     for n in ("aal_eal_fwd_bwd", "aal_wtv_fwd_bwd", "aal_sim_accept_grpo", "aal_workspace_bytes",
               "aal_loss_fwd_bwd", "aal_loss_workspace_bytes", "aal_grpo_fwd_bwd", "aal_grpo_workspace_bytes",
               "aal_status_string", "aal_last_error", "aal_version", "aal_vp_row_partials", "aal_vp_merge_rows",
-              "aal_vp_accept_partials", "aal_vp_window_scan", "aal_vp_sequence_scan", "aal_vp_grad"):
+              "aal_vp_accept_partials", "aal_vp_window_scan", "aal_vp_sequence_scan", "aal_vp_grad",
+              "aal_eal_fwd_bwd_ex", "aal_wtv_fwd_bwd_ex", "aal_sim_accept_grpo_ex"):
         assert n in names
+
+
+# The six calls of the boundary with their exact C types: each line assigns the
+# declared function to a pointer of the stated type, and the C compiler
+# rejects any mismatch (-Werror).  The `_ex` calls add the schedule flags (and
+# the simulation's per-position accept output) beside these, unchanged.
+BOUNDARY_SIGNATURES = '''
+size_t (*f_ws)(int64_t, int64_t) = aal_workspace_bytes;
+const char* (*f_ss)(aal_status_t) = aal_status_string;
+const char* (*f_le)(void) = aal_last_error;
+aal_status_t (*f_eal)(const void*, const void*, aal_dtype_t, int64_t, int32_t, int32_t, float,
+                      float*, float*, float*, int32_t*, void*, aal_dtype_t, const float*,
+                      void*, size_t, hipStream_t) = aal_eal_fwd_bwd;
+aal_status_t (*f_wtv)(const void*, const void*, aal_dtype_t, int64_t, int32_t, int32_t, float, float,
+                      float*, float*, float*, void*, aal_dtype_t, const float*,
+                      void*, size_t, hipStream_t) = aal_wtv_fwd_bwd;
+aal_status_t (*f_sim)(const void*, const void*, aal_dtype_t, int32_t, int32_t, int32_t, int32_t, float,
+                      const float*, const float*, int32_t*, int32_t*, float*, float, int32_t, float,
+                      void*, size_t, hipStream_t) = aal_sim_accept_grpo;
+_Static_assert(AAL_BF16 == 0 && AAL_F32 == 1, "dtype codes");
+_Static_assert(AAL_OK == 0 && AAL_ERR_ARG == 1 && AAL_ERR_DTYPE == 2 && AAL_ERR_ALIGN == 3 &&
+               AAL_ERR_WORKSPACE == 4 && AAL_ERR_HIP == 5, "status codes");
+'''
+
+
+def test_boundary_signatures_are_exact(tmp_path):
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "boundary.c"
+    src.write_text('#include "aal.h"\n' + BOUNDARY_SIGNATURES)
+    r = subprocess.run([cc, "-std=c11", "-Werror", "-Wall", "-fsyntax-only", f"-I{os.path.join(ROOT, 'include')}",
+                        str(src)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    # the header still compiles after HIP's own declaration of hipStream_t (C++)
+    cxx = shutil.which("g++")
+    if cxx:
+        src2 = tmp_path / "twice.cc"
+        src2.write_text('typedef struct ihipStream_t* hipStream_t;\n#include "aal.h"\nint main() { return 0; }\n')
+        r = subprocess.run([cxx, "-std=c++17", "-Werror", "-fsyntax-only", f"-I{os.path.join(ROOT, 'include')}",
+                            str(src2)], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -61,7 +106,7 @@ def _eal(L, **kw):
     args = dict(zd=16, zt=16, dt=0, N=2, K=3, V=8, T=1.0, loss=16, grad=None, gdt=0, ws=256, wsb=1 << 30)
     args.update(kw)
     return L.aal_eal_fwd_bwd(args["zd"], args["zt"], args["dt"], args["N"], args["K"], args["V"], args["T"],
-                             args["loss"], None, None, None, args["grad"], args["gdt"], None, 0, args["ws"],
+                             args["loss"], None, None, None, args["grad"], args["gdt"], None, args["ws"],
                              args["wsb"], None)
 
 
@@ -79,15 +124,19 @@ def test_eal_validation(lib, kw, code):
 
 def test_wtv_and_sim_validation(lib):
     L = lib.lib()
-    st = L.aal_wtv_fwd_bwd(16, 16, 0, 2, 3, 8, 1.0, 0.0, 16, None, None, None, 0, None, 0, 256, 1 << 30, None)
+    st = L.aal_wtv_fwd_bwd(16, 16, 0, 2, 3, 8, 1.0, 0.0, 16, None, None, None, 0, None, 256, 1 << 30, None)
     assert st == 1 and b"temp_target" in L.aal_last_error()
-    st = L.aal_wtv_fwd_bwd(16, 16, 0, 2, 3, 8, 1.0, 1.0, 16, None, None, None, 0, None, 4, 256, 1 << 30, None)
+    st = L.aal_wtv_fwd_bwd_ex(16, 16, 0, 2, 3, 8, 1.0, 1.0, 16, None, None, None, 0, None, 4, 256, 1 << 30, None)
     assert st == 1 and b"flags" in L.aal_last_error()
+    st = L.aal_eal_fwd_bwd_ex(16, 16, 0, 2, 3, 8, 1.0, 16, None, None, None, None, 0, None, 2, 256, 1 << 30, None)
+    assert st == 1 and b"flags" in L.aal_last_error()
+    st = L.aal_eal_fwd_bwd_ex(16, 16, 0, 0, 3, 8, 1.0, 16, None, None, None, None, 0, None, 1, 256, 1 << 30, None)
+    assert st == 1 and b"N must" in L.aal_last_error()
 
     def sim(**kw):
         a = dict(P=2, G=4, K=3, V=10, T=1.0, u1=16, rew=16, eps=1e-6, ddof=0, ws=256, wsb=1 << 30)
         a.update(kw)
-        return L.aal_sim_accept_grpo(16, 16, 0, a["P"], a["G"], a["K"], a["V"], a["T"], a["u1"], 16, None, None,
+        return L.aal_sim_accept_grpo(16, 16, 0, a["P"], a["G"], a["K"], a["V"], a["T"], a["u1"], 16, None,
                                      a["rew"], 16, a["eps"], a["ddof"], 0.0, a["ws"], a["wsb"], None)
     assert sim(u1=None) == 1
     assert sim(rew=None) == 1
@@ -97,6 +146,9 @@ def test_wtv_and_sim_validation(lib):
     assert sim(eps=-1.0) == 1
     assert sim(wsb=8) == 4
     assert sim(ws=8) == 3
+    st = L.aal_sim_accept_grpo_ex(16, 16, 0, 2, 4, 3, 10, 1.0, None, 16, None, None, 16, 16, 1e-6, 0, 0.0, 256,
+                                  1 << 30, None)
+    assert st == 1 and b"u1" in L.aal_last_error()
 
 
 def test_loss_workspace_bytes(lib):
@@ -168,14 +220,16 @@ def test_vp_validation(lib):
     L = lib.lib()
     P = L.aal_vp_row_partials
 
-    def part(zd=16, zt=16, lab=None, dt=0, rows=2, vs=8, v0=0, mode=0, td=1.0, tt=1.0, parts=16):
-        return P(zd, zt, lab, dt, rows, vs, v0, mode, td, tt, parts, None)
+    def part(zd=16, zt=16, lab=None, dt=0, rows=2, vs=8, v0=0, vtot=None, mode=0, td=1.0, tt=1.0, parts=16):
+        vtot = v0 + vs if vtot is None else vtot
+        return P(zd, zt, lab, dt, rows, vs, v0, vtot, mode, td, tt, parts, None)
 
     for kw, code in [(dict(rows=0), 1), (dict(vs=0), 1), (dict(v0=-1), 1), (dict(v0=(1 << 31) - 4), 1),
                      (dict(dt=5), 2), (dict(zd=18), 3), (dict(zt=None), 1), (dict(mode=9), 1),
                      (dict(mode=1, tt=0.0), 1), (dict(td=float("nan")), 1), (dict(parts=None), 1),
                      (dict(parts=18), 3), (dict(rows=1 << 60), 1), (dict(lab=16, mode=1), 1),
-                     (dict(lab=18), 3), (dict(lab=16, zd=None), 1)]:
+                     (dict(lab=18), 3), (dict(lab=16, zd=None), 1), (dict(v0=8, vtot=15), 1),
+                     (dict(vtot=0), 1)]:
         assert part(**kw) == code, kw
         assert L.aal_last_error().decode() != ""
     M = L.aal_vp_merge_rows

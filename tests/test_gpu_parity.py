@@ -175,6 +175,34 @@ def test_argmax_ties_lowest_index(A, dev):
         assert np.array_equal(xs, O.greedy_token(host64(b)))
 
 
+@pytest.mark.parametrize("path", ["auto", "stream"])
+@pytest.mark.parametrize("dtype", [BF16, F32])
+def test_argmax_ties_across_team_members(A, dev, dtype, path):
+    """Tied greedy maxima at V = 128256 placed in different members of a
+    resident team (8192 bf16 / 4096 fp32 columns per member at K = 7), at
+    member boundaries and in different waves of one member: the lowest index
+    wins in both schedules."""
+    N, K, V = 3, 7, 128256
+    zd, zt = _inputs("c2", (N, K, V), F32, seed=31, dev="cpu")
+    ties = [(0, 0, [100, 125000]),            # member 0 and the last member
+            (0, 1, [125000, 128255]),         # both in the last member, the second at the row end
+            (0, 2, [8191, 8192]),             # either side of the first member boundary
+            (0, 3, [4095, 4096, 70000]),      # member boundaries at fp32 widths
+            (1, 0, [24576, 127000, 3]),       # three members, the lowest index listed last
+            (1, 6, [64, 512, 1024, 128000]),  # different waves and members
+            (2, 4, list(range(0, V, 8192)))]  # one tie in every bf16 member
+    for n, k, cols in ties:
+        zt[n, k, cols] = 40.0
+    a, b = zd.to(dtype).to(dev), zt.to(dtype).to(dev)
+    r = A.aal_eal_fwd_bwd(a, b, 1.0, flags=_flags(A, path))
+    torch.cuda.synchronize()
+    xs = r["xstar"].cpu().numpy()
+    for n, k, cols in ties:
+        assert xs[n, k] == min(cols), (n, k, xs[n, k])
+    assert np.array_equal(xs, O.greedy_token(host64(b)))
+    _check_eal(A, a, b, 1.0, dtype, _flags(A, path))
+
+
 def test_forward_only_and_stream_and_determinism(A, dev):
     zd, zt = _inputs("c2", (5, 7, 4096), BF16, seed=9, dev=dev)
     s = torch.cuda.Stream()

@@ -50,7 +50,8 @@ def run_vp(A, zd, zt, mode, widths, Td=1.0, Tt=1.0, gdtype=None, scale=None, lab
     rows = N * K
     sl = [(v0, w, zd.reshape(rows, V)[:, v0:v0 + w].contiguous(), zt.reshape(rows, V)[:, v0:v0 + w].contiguous())
           for v0, w in _bounds(V, widths)]
-    parts = torch.stack([A.aal_vp_row_partials(d, None if labels is not None else t, v0, mode, Td, Tt, labels=labels)
+    parts = torch.stack([A.aal_vp_row_partials(d, None if labels is not None else t, v0, mode, Td, Tt, V_total=V,
+                                               labels=labels)
                          for v0, w, d, t in sl])
     row = A.aal_vp_merge_rows(parts, mode, Td, Tt)
     acc = None
@@ -168,11 +169,13 @@ def test_vp_argument_errors(A, dev):
     zd, zt = _inputs("c2", (2, 3, 64), BF16, seed=1, dev=dev)
     d, t = zd.reshape(6, 64).contiguous(), zt.reshape(6, 64).contiguous()
     with pytest.raises(A.AalError):
-        A.aal_vp_row_partials(d, t, -1, A.AAL_VP_EAL)
+        A.aal_vp_row_partials(d, t, -1, A.AAL_VP_EAL, V_total=64)
     with pytest.raises(A.AalError):
-        A.aal_vp_row_partials(d, t, 0, 7)
+        A.aal_vp_row_partials(d, t, 0, 7, V_total=64)
     with pytest.raises(A.AalError):
-        A.aal_vp_row_partials(d, t, 0, A.AAL_VP_WTV, 1.0, 0.0)
+        A.aal_vp_row_partials(d, t, 0, A.AAL_VP_WTV, 1.0, 0.0, V_total=64)
+    with pytest.raises(A.AalError):
+        A.aal_vp_row_partials(d, t, 8, A.AAL_VP_EAL, V_total=64)  # the slice ends past V_total
 
 
 @pytest.mark.parametrize("mode", ["wtv", "eal"])
@@ -243,13 +246,40 @@ def test_vp_eal_labels(A, dev, dtype, widths):
     check_grad(host64(r["grad"]), o["grad"], o["coef_eal"], zd.dtype, F32)
 
 
+@pytest.mark.parametrize("widths", [[256, 256, 256, 256], [300, 301, 399]])
+def test_vp_eal_labels_out_of_range_match_fused_call(A, dev, widths):
+    """Labels outside [0, V) (an ignore index of -100, -1, V, V + 7) are clamped
+    into the vocabulary exactly as aal_loss_fwd_bwd clamps them: the assembled
+    vocabulary-parallel loss, E, acceptances, tokens and gradient equal the
+    fused call's on the same labels."""
+    N, K, V = 4, 3, sum(widths)
+    zd, zt = _inputs("c2", (N, K, V), F32, seed=23, dev=dev)
+    g = torch.Generator().manual_seed(5)
+    lab = torch.randint(0, V, (N * K,), generator=g, dtype=torch.int32)
+    lab[:5] = torch.tensor([-100, -1, V, V + 7, (1 << 31) - 1], dtype=torch.int32)
+    lab_d = lab.to(dev)
+    r = run_vp(A, zd, zt, A.AAL_VP_EAL, widths, 0.9, 1.0, F32, labels=lab_d)
+    f = A.aal_loss_fwd_bwd(zd, zt, K, weights=(0.0, 1.0, 0.0, 0.0), temp_draft=0.9, labels=lab_d,
+                           grad_dtype=F32)
+    torch.cuda.synchronize()
+    clamped = lab.clamp(0, V - 1).numpy()
+    assert np.array_equal(r["xstar"].cpu().numpy().reshape(-1), clamped)
+    assert np.array_equal(f["xstar"].cpu().numpy().reshape(-1), clamped)
+    assert rel_err(r["loss"].item(), f["loss"].item()) <= 1e-5
+    np.testing.assert_allclose(host64(r["E"]), host64(f["E_eal"]), rtol=1e-5)
+    np.testing.assert_allclose(host64(r["accept"]).reshape(-1), host64(f["accept_eal"]), rtol=1e-5, atol=1e-7)
+    o = O.combined_loss(host64(zd), host64(zt), 0.9, 1.0, (0.0, 1.0, 0.0, 0.0), 0, N, K, K, labels=clamped)
+    check_grad(host64(r["grad"]), o["grad"], o["coef_eal"], zd.dtype, F32)
+    check_grad(host64(f["grad"]), o["grad"], o["coef_eal"], zd.dtype, F32)
+
+
 def run_vp_seq(A, zd, zt, mode, widths, K, Td=1.0, Tt=1.0, gdtype=None, scale=None):
     """The vocabulary-parallel steps over B sequences [B, S, V] with windows sliding by one."""
     B, S, V = zd.shape
     rows = B * S
     sl = [(v0, w, zd.reshape(rows, V)[:, v0:v0 + w].contiguous(), zt.reshape(rows, V)[:, v0:v0 + w].contiguous())
           for v0, w in _bounds(V, widths)]
-    parts = torch.stack([A.aal_vp_row_partials(d, t, v0, mode, Td, Tt) for v0, w, d, t in sl])
+    parts = torch.stack([A.aal_vp_row_partials(d, t, v0, mode, Td, Tt, V_total=V) for v0, w, d, t in sl])
     row = A.aal_vp_merge_rows(parts, mode, Td, Tt)
     acc = None
     if mode == A.AAL_VP_WTV:
