@@ -167,6 +167,39 @@ aal_status_t aal_wtv_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_d
                                 uint32_t flags, void* workspace, size_t workspace_bytes,
                                 hipStream_t stream);
 
+/* Bytes of the static device scratch that aal_wtv_fwd_bwd_noalloc uses on
+ * each GPU (32 MiB): it serves any N, K with aal_workspace_bytes(N*K, N) at
+ * most this size, i.e. N*K*32 + N*4 bytes plus 4 MiB, rounded up to 256-byte
+ * pieces (at least 815,000 logit rows at any K). */
+#define AAL_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/*
+ * aal_wtv_fwd_bwd for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation, kernels and results as aal_wtv_fwd_bwd, with the
+ * workspace taken from a static device array of AAL_NOALLOC_SCRATCH_BYTES
+ * inside the library instead of an argument.  It calls no hipMalloc, hipFree
+ * or allocating library routine.  The array's address on a device is looked
+ * up on the first call on that device (hipGetSymbolAddress), so that first
+ * call must not be made while a graph is being captured.
+ *
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents (each call clears what must start at zero itself): calls that
+ * overlap on one GPU -- on different streams, or from different host threads
+ * without ordering -- race and give undefined results.  Calls on different
+ * GPUs do not share memory.
+ *
+ * Arguments, outputs and validation as for aal_wtv_fwd_bwd, minus the
+ * workspace; a size whose workspace would exceed AAL_NOALLOC_SCRATCH_BYTES
+ * gives AAL_ERR_WORKSPACE before anything is enqueued.
+ */
+aal_status_t aal_wtv_fwd_bwd_noalloc(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
+                                     int64_t N, int32_t K, int32_t V,
+                                     float temp_draft, float temp_target,
+                                     float* loss, float* eal_per_window, float* accept,
+                                     void* grad_draft, aal_dtype_t grad_dtype, const float* grad_scale,
+                                     hipStream_t stream);
+
 /*
  * Simulated acceptance length and group-relative advantage (Section "GRPO
  * Loss on Acceptance Length": the accepted-length count and Eq. advantage;

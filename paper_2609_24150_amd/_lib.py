@@ -19,6 +19,7 @@ AAL_ERR_ALIGN = 3
 AAL_ERR_WORKSPACE = 4
 AAL_ERR_HIP = 5
 AAL_FLAG_STREAMING = 1
+AAL_NOALLOC_SCRATCH_BYTES = 32 << 20
 AAL_LAYOUT_WINDOWS = 0
 AAL_LAYOUT_SEQUENCES = 1
 AAL_VP_EAL = 0
@@ -66,6 +67,11 @@ _SIGNATURES = {
         _vp, _vp, _vp,
         _vp, C.c_int, _vp,
         C.c_uint32, _vp, C.c_size_t, _vp]),
+    "aal_wtv_fwd_bwd_noalloc": (C.c_int, [
+        _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_float, C.c_float,
+        _vp, _vp, _vp,
+        _vp, C.c_int, _vp,
+        _vp]),
     "aal_sim_accept_grpo": (C.c_int, [
         _vp, _vp, C.c_int, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_float,
         _vp, _vp, _vp, _vp, _vp,

@@ -8,6 +8,14 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
+
+// Device scratch of aal_wtv_fwd_bwd_noalloc: a file-scope array in the code
+// object, so that entry point never allocates.  Each GPU holds its own copy
+// at its own address until the process ends.  Host code never uses the name
+// as an address: it takes the per-device address from hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[AAL_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 // A plain per-thread buffer: nothing to construct or destroy at thread or
@@ -123,6 +131,31 @@ aal_status_t vp_scales(int mode, float temp_draft, float temp_target, float* scd
 }
 
 aal::Mode vp_mode(int m) { return m == AAL_VP_EAL ? aal::Mode::kEal : aal::Mode::kWtv; }
+
+// Per-device address of `scratch`, looked up once per device with that device
+// current (0 = not yet looked up).  Atomics: nothing to destroy at exit.
+constexpr int kMaxScratchDevices = 64;
+std::atomic<uintptr_t> g_scratch_addr[kMaxScratchDevices];
+
+aal_status_t scratch_for_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "hipGetDevice failed: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(AAL_ERR_ARG, "device %d is beyond the %d devices the static scratch serves", dev,
+                kMaxScratchDevices);
+  uintptr_t a = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (a == 0) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(AAL_ERR_HIP, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev, hipGetErrorString(e));
+    a = reinterpret_cast<uintptr_t>(p);
+    g_scratch_addr[dev].store(a, std::memory_order_release);
+  }
+  *out = reinterpret_cast<void*>(a);
+  return AAL_OK;
+}
 
 }  // namespace
 
@@ -300,6 +333,28 @@ aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_
                                  hipStream_t stream) {
   return aal_sim_accept_grpo_ex(z_draft, z_target, in_dtype, P, G, K, V, temperature, u1, u2, draft_token, nullptr,
                                 reward, advantage, eps, std_ddof, adv_clip, workspace, workspace_bytes, stream);
+}
+
+aal_status_t aal_wtv_fwd_bwd_noalloc(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N,
+                                     int32_t K, int32_t V, float temp_draft, float temp_target, float* loss,
+                                     float* eal_per_window, float* accept, void* grad_draft, aal_dtype_t grad_dtype,
+                                     const float* grad_scale, hipStream_t stream) {
+  clear_error();
+  if (N < 1) return fail(AAL_ERR_ARG, "N must be >= 1 (got %lld)", (long long)N);
+  if (K < 1 || K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", K);
+  if (N > (int64_t(1) << 31) / K) return fail(AAL_ERR_ARG, "N*K must be < 2^31");
+  const size_t need = aal::workspace_bytes(N * K, N);
+  if (need > size_t(AAL_NOALLOC_SCRATCH_BYTES))
+    return fail(AAL_ERR_WORKSPACE,
+                "aal_wtv_fwd_bwd_noalloc: N=%lld, K=%d needs %zu bytes of scratch, more than the %zu bytes of "
+                "the static scratch buffer",
+                (long long)N, K, need, size_t(AAL_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  const aal_status_t st = scratch_for_current_device(&ws);
+  if (st != AAL_OK) return st;
+  return aal_wtv_fwd_bwd_ex(z_draft, z_target, in_dtype, N, K, V, temp_draft, temp_target, loss, eal_per_window,
+                            accept, grad_draft, grad_dtype, grad_scale, 0u, ws, size_t(AAL_NOALLOC_SCRATCH_BYTES),
+                            stream);
 }
 
 size_t aal_loss_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32_t K) {
