@@ -15,8 +15,11 @@
 //            payload; published, merged in member order (bit-identical row
 //            constants in every member).  With labels, x* is the label and
 //            both logits at it are read once per row.
-//   phase B  (WTV, TV or KL term) partial sums of min(p, q), of q over
-//            q < p, and of p (log p - log q); published, merged.
+//   phase B  (WTV or TV term) partial sums of min(p, q), of q over q < p,
+//            and with a KL term of p (log p - log q); published, merged.
+//            Without a WTV or TV term there is no phase B: the KL partials
+//            are summed in phase C and merged one chunk later (the KL value
+//            enters the loss, not the gradient).
 //   scan     with windows sliding over a sequence, a row's coefficient needs
 //            the acceptances of the K-1 rows on either side: one member per
 //            team publishes the chunk's a values (tagged words, written once
@@ -92,6 +95,14 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   // (a WTV or TV term, or the a_tv / E_tv outputs).
   constexpr bool PQ = (VAR & 1) != 0, KL = (VAR & 2) != 0, AM = (VAR & 4) != 0, TV = (VAR & 8) != 0;
   static_assert(PQ || !(KL || TV), "KL and TV need the target normaliser");
+  // Without a WTV or TV term there is no phase B: the KL term's per-row
+  // partials are accumulated in phase C from the two exponentials the
+  // gradient evaluates anyway (the KL value enters the loss only, never the
+  // gradient), and merged over the team one chunk later, inside the next
+  // chunk's phase-A merge (the team's last chunk after the loop).
+  constexpr bool KLC = KL && !TV;
+  constexpr bool HB = TV;  // a phase B
+  constexpr int kKlWord = 12;  // slot word of the KL partials (phase B is absent)
   constexpr int kBlock = kGenBlock;
   constexpr int kWaves = kBlock / kWave;
   constexpr int E = TI::kVec;
@@ -112,6 +123,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   __shared__ float sh_a[3 * K][2];  // a_tv, a_eal of rows row0 - K .. row0 + 2K - 1
   __shared__ float sh_coef[K][7];   // cA, cB, cP scaled by 2^-l2s_d; cX; cA, cB, cP unscaled
   __shared__ float sh_d[K][K][2];   // dE/da (WTV, EAL) of row k at place jj of a window
+  __shared__ float sh_klw[2][kWaves][K];  // KLC: each wave's KL partials, by chunk parity
 
   const int b = blockIdx.x;
   int team, member;
@@ -192,10 +204,13 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   const double gscale = p.grad_scale ? double(*p.grad_scale) : 1.0;
   const double inv_k = 1.0 / double(K);
   uint32_t iter = 0;
+  int64_t prev_row0 = 0;  // the previous chunk (KLC: its KL is merged one chunk later)
+  int prev_nvalid = 0;
   for (; c < p.NC; c += p.T, ++iter) {
     const int parity = iter & 1;
     const uint32_t tagA = 2u * (iter + 1u), tagB = tagA + 1u;
     uint64_t* const slots = slots_team + parity * slot_plane;
+    uint64_t* const prev_slots = slots_team + (parity ^ 1) * slot_plane;
     int64_t row0;
     int j, nvalid;
     chunk(c, row0, j, nvalid);
@@ -374,6 +389,17 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         }
       }
       lds_barrier();
+      if constexpr (KLC && k0 == 0) {
+        // the previous chunk's KL partials of this member: every wave finished
+        // that chunk's phase C before this barrier; summed over the waves in
+        // order and published with the previous chunk's tag
+        if (iter > 0 && tid < K) {
+          float r = sh_klw[parity ^ 1][0][tid];
+#pragma unroll
+          for (int i = 1; i < kWaves; ++i) r += sh_klw[parity ^ 1][i][tid];
+          publish(prev_slots + (int64_t(tid) * p.W + member) * kGenSlotWords + kKlWord, r, 2u * iter);
+        }
+      }
       if (tid < kC * KG) {
         const int k = k0 + tid / kC, cc = tid % kC;
         float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
@@ -442,6 +468,21 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           sh_x[k] = x;
           sh_row[k][4] = aq;
           sh_row[k][5] = px;
+        }
+        if constexpr (KLC) {
+          // the previous chunk's KL of row k: the members' partials in order,
+          // then the wave; they were published before this chunk's phase-A
+          // words, so the polls find them at once
+          if (member == 0 && iter > 0) {
+            float r[1] = {0.f};
+            for (int jm = lane; jm < p.W; jm += kWave) {
+              float q[1];
+              collect<1>(prev_slots + (int64_t(k) * p.W + jm) * kGenSlotWords + kKlWord, 2u * iter, p.err, q);
+              r[0] += q[0];
+            }
+            wave_sum_n(r);
+            if (lane == 0 && k < prev_nvalid) p.stats[prev_row0 + k].kl = r[0];
+          }
         }
       }
     };
@@ -560,7 +601,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
     if constexpr (K0 < K) phase_a(IK0{}, IK{});
 
     // ------------------------------------------------------------ phase B
-    if constexpr (!PQ) {
+    if constexpr (!HB) {
       merge_a(0, K);
       if (tid < K) {
         sh_b[tid][0] = 0.f;
@@ -685,7 +726,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       sh_coef[k][6] = cP;
       if (member == 0) {
         const int64_t r = row0 + k;
-        p.stats[r].kl = sh_b[k][2];
+        if constexpr (!KLC) p.stats[r].kl = sh_b[k][2];
         p.stats[r].tv_w = float(count * (1.0 - a_tv));
         if (p.accept_tv) p.accept_tv[r] = sh_b[k][0];
         if (p.accept_eal) p.accept_eal[r] = sh_row[k][4];
@@ -696,6 +737,12 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
 
     // ------------------------------------------------------------ phase C
     uint8_t* const gw = p.grad ? p.grad + row0 * int64_t(p.grow_bytes) : nullptr;
+    // KLC: this thread's sum of 2^t (t - u) over row k's entries
+    // (p (log2 p - log2 q) 2^l2s_d), reduced over the wave as soon as the
+    // row's last pair is done, so at most two of them are live
+    float klp[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) klp[k] = 0.f;
     wait_vmem_all();  // staging has landed
     pin_all();
 #pragma unroll
@@ -722,7 +769,11 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           } else {
             g[e] = ex2(u) * cA;  // no mask without a TV term: cA = cB
           }
-          if constexpr (KL) g[e] = __builtin_fmaf(cP, ex2(t), g[e]);
+          if constexpr (KL) {
+            const float ep = ex2(t);  // p 2^l2s_d; p = 0 contributes nothing
+            g[e] = __builtin_fmaf(cP, ep, g[e]);
+            if constexpr (KLC) klp[k] = __builtin_fmaf(ep, ep > 0.f ? t - u : 0.f, klp[k]);
+          }
         }
       } else {
 #pragma unroll
@@ -736,6 +787,17 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       } else {
         rd[k][v] = bld16(nd, coff[v], k * p.row_bytes);
         rt[k][v] = bld16(nt, coff[v], k * p.row_bytes);
+      }
+      if constexpr (KLC) {
+        // the last pair of row k in this order: (jp + kPre) % kPairs runs
+        // through the pairs from kPre, wrapping round, so a row that pair kPre
+        // cuts (kPre not a multiple of NV) ends at pair kPre - 1
+        constexpr int kCut = kPre % NV != 0 ? (kPre - 1) / NV : -1;
+        const bool row_done = k == kCut ? i == kPre - 1 : v == NV - 1;
+        if (row_done) {
+          const float r = wave_sum(klp[k]);  // this wave's partial of row k (uniform)
+          if (lane == 0) sh_klw[parity][wv][k] = r * ex2(-sh_row[k][1]) * kLn2;
+        }
       }
     }
     if (eal && gw != nullptr) {
@@ -756,12 +818,41 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         }
       }
     }
+    prev_row0 = row0;
+    prev_nvalid = nvalid;
     // No barrier before the next chunk: a wave only reads and restages its
     // own slice of the staging buffer (after its reads above have completed),
-    // the label data is double-buffered, and the shared row constants are
-    // rewritten only after the barrier closing the next chunk's first
-    // phase-A group, which every wave reaches after finishing this phase C.
+    // the label data and the KL partials are double-buffered, and the shared
+    // row constants are rewritten only after the barrier closing the next
+    // chunk's first phase-A group, which every wave reaches after finishing
+    // this phase C.
     wait_lds_all();
+  }
+  if constexpr (KLC) {
+    // the team's last chunk: its KL partials, published and merged as above
+    if (iter > 0) {
+      const int pp = int((iter - 1) & 1);
+      uint64_t* const last_slots = slots_team + pp * slot_plane;
+      lds_barrier();
+      if (tid < K) {
+        float r = sh_klw[pp][0][tid];
+#pragma unroll
+        for (int i = 1; i < kWaves; ++i) r += sh_klw[pp][i][tid];
+        publish(last_slots + (int64_t(tid) * p.W + member) * kGenSlotWords + kKlWord, r, 2u * iter);
+      }
+      if (member == 0) {
+        for (int k = wv; k < K; k += kWaves) {
+          float r[1] = {0.f};
+          for (int jm = lane; jm < p.W; jm += kWave) {
+            float q[1];
+            collect<1>(last_slots + (int64_t(k) * p.W + jm) * kGenSlotWords + kKlWord, 2u * iter, p.err, q);
+            r[0] += q[0];
+          }
+          wave_sum_n(r);
+          if (lane == 0 && k < prev_nvalid) p.stats[prev_row0 + k].kl = r[0];
+        }
+      }
+    }
   }
   wait_vmem_all();
 }
