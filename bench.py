@@ -31,6 +31,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+SIMDS = 1024          # 256 CUs x 4 SIMDs
+CLOCK_HZ = 2.4e9      # MI355X peak engine clock
 HOST_CPU_SHARE = 16
 PMC_PROFILE = os.path.join(ROOT, "profiles", "resident_wtv_c2_pmc.txt")
 KERNEL_SOURCES = ["paper_2609_24150_amd/csrc/aal_resident.hip", "paper_2609_24150_amd/csrc/aal_resident_common.h",
@@ -101,13 +103,14 @@ def _cpu_model() -> str:
     return "unknown"
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch of the fused kernel from the committed rocprofv3
-    FETCH_SIZE / WRITE_SIZE summary, or None when that summary does not cover
-    this workload or the kernel sources changed since it was taken."""
+def profile_fields(workload: str) -> dict:
+    """Per-launch figures of the fused kernel from the committed rocprofv3
+    summary (HBM traffic from FETCH_SIZE / WRITE_SIZE, VALU instruction and
+    issue-cycle counts), or {} when that summary does not cover this workload
+    or the kernel sources changed since it was taken."""
     import hashlib
     if workload != "c2" or not os.path.exists(PMC_PROFILE):
-        return None
+        return {}
     fields = {}
     for line in open(PMC_PROFILE):
         if ":" in line and not line.startswith("#"):
@@ -117,11 +120,37 @@ def measured_traffic(workload: str):
     for src in KERNEL_SOURCES:
         h.update(open(os.path.join(ROOT, src), "rb").read())
     if fields.get("kernel_source_sha256") != h.hexdigest():
+        return {}
+    return fields
+
+
+def alu_roofline(fields: dict, ms: float, alg_bytes: float):
+    """The VALU roofline of the fused kernel: its VALU instructions per launch
+    (SQ_INSTS_VALU) over the measured time, against the issue rate of 1024
+    SIMDs at 2.4 GHz for this kernel's own instruction mix.  A wave64 VALU
+    instruction occupies a 16-lane SIMD for 4 cycles; the counters give the
+    mix's average, 4 SQ_ACTIVE_INST_VALU / SQ_INSTS_VALU cycles (v_exp_f32
+    takes about 8).  frac is then the fraction of the SIMDs' cycles spent
+    issuing VALU work, and floor_ms the time at 100%."""
+    if "valu_instructions_per_launch" not in fields:
         return None
-    return float(fields["traffic_bytes_per_launch"])
+    valu = float(fields["valu_instructions_per_launch"])
+    cycles = 4.0 * float(fields["valu_active_quad_cycles_per_launch"])
+    cpi = cycles / valu
+    peak = SIMDS * CLOCK_HZ / cpi
+    achieved = valu / (ms * 1e-3)
+    floor_s = cycles / SIMDS / CLOCK_HZ
+    return {"bound": "alu", "achieved": achieved / 1e9, "peak": peak / 1e9, "unit": "G VALU wave-instructions/s",
+            "frac": achieved / peak, "cycles_per_instruction": cpi, "valu_instructions_per_launch": valu,
+            "floor_ms": floor_s * 1e3, "hbm_frac_at_alu_floor": alg_bytes / floor_s / 1e9 / HBM_PEAK_GBPS,
+            "counters": "profiles/resident_wtv_c2_pmc.txt"}
 
 
 # ----------------------------------------------------------------- GPU legs
+def _progress(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def _time_calls(fn, steps, warmup, stream):
     import torch
     for _ in range(warmup):
@@ -134,7 +163,9 @@ def _time_calls(fn, steps, warmup, stream):
         fn()
     stop.record(stream)
     torch.cuda.synchronize()
-    return start.elapsed_time(stop) / steps  # ms per call
+    ms = start.elapsed_time(stop) / steps  # ms per call
+    _progress(f"timed {steps} calls: {ms:.4f} ms each")
+    return ms
 
 
 def _fail(msg):
@@ -403,6 +434,8 @@ def main():
     del outs
     alg_bytes = rows * (2 * s_in + s_g) * V
     achieved = alg_bytes / (ms * 1e-3) / 1e9
+    prof = profile_fields(args.workload)
+    traffic = float(prof["traffic_bytes_per_launch"]) if "traffic_bytes_per_launch" in prof else None
     out = {
         "metric": "EAL/WTV fwd+bwd logit rows/s + % of HBM peak, V=128256 bf16, 1 GPU",
         "value": rows / (ms * 1e-3),
@@ -419,10 +452,11 @@ def main():
         "config": {"workload": WORKLOAD_TEXT[args.workload], "N": N, "K": K, "V": V,
                    "windows_per_s": N / (ms * 1e-3)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": measured_traffic(args.workload),
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
                      "algorithmic_bytes": alg_bytes,
                      "kernel": "k_resident (timed: the whole aal_wtv_fwd_bwd call, i.e. k_resident plus "
-                               "three microsecond-scale set-up/reduction kernels)"},
+                               "three microsecond-scale set-up/reduction kernels)",
+                     "alu": alu_roofline(prof, ms, alg_bytes)},
         "cpu_baseline": cpu,
         "validation": valid,
         "practical_ceilings": ceilings(dev),
