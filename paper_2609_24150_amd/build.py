@@ -1,6 +1,8 @@
 """Build libaal.so (HIP, gfx950) in-tree with hipcc.
 
-    python -m paper_2609_24150_amd.build        # compile every source, link
+    python -m paper_2609_24150_amd.build              # compile every source, link
+    python -m paper_2609_24150_amd.build --sanitize   # also the C-ABI layer's host code with
+                                                      # AddressSanitizer + UBSan (_build/aal_api_asan.o)
 
 Each .hip source compiles to an object in parallel, then one shared library
 is linked next to this file.  Device code is built with packed-fp32
@@ -53,6 +55,26 @@ def _compile(src: str) -> str:
     return obj
 
 
+# Host-side sanitizers for the C-ABI layer (argument validation, workspace
+# carve-up, dispatch).  Each -fsanitize= applies to the host compilation only:
+# device code is never built with them.
+SANITIZE_FLAGS = ["-O1", "-g", "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                  "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def compile_api_sanitized(obj: str | None = None) -> str:
+    """Compile csrc/aal_api.hip with the host sanitizers into an object that a
+    driver links with host-side stand-ins for the kernel launchers."""
+    os.makedirs(BUILD, exist_ok=True)
+    obj = obj or os.path.join(BUILD, "aal_api_asan.o")
+    flags = [f for f in COMMON_FLAGS if f != "-O3"] + SANITIZE_FLAGS
+    cmd = [hipcc(), *flags, "-c", os.path.join(CSRC, "aal_api.hip"), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    return obj
+
+
 def build(verbose: bool = True) -> str:
     os.makedirs(BUILD, exist_ok=True)
     srcs = sources()
@@ -71,4 +93,6 @@ def build(verbose: bool = True) -> str:
 
 if __name__ == "__main__":
     build()
+    if "--sanitize" in sys.argv[1:]:
+        print(f"built {compile_api_sanitized()}")
     sys.exit(0)

@@ -44,6 +44,17 @@ bool positive_finite(float x) {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
+// The integer held by an enum argument, read without loading it as the enum
+// type: a C caller may pass any int, and values outside the enumerators are
+// validated here rather than assumed away.
+template <class E>
+int raw(const E& e) {
+  static_assert(sizeof(E) == sizeof(int), "enum arguments are int-sized");
+  int v;
+  memcpy(&v, &e, sizeof v);
+  return v;
+}
+
 bool valid_dtype(int d) { return d == AAL_BF16 || d == AAL_F32; }
 
 aal::DType to_dtype(int d) { return d == AAL_BF16 ? aal::DType::kBf16 : aal::DType::kF32; }
@@ -169,7 +180,7 @@ size_t aal_workspace_bytes(int64_t rows, int64_t windows) {
 }
 
 const char* aal_status_string(aal_status_t status) {
-  switch (int(status)) {
+  switch (raw(status)) {
     case AAL_OK: return "AAL_OK";
     case AAL_ERR_ARG: return "AAL_ERR_ARG: invalid argument";
     case AAL_ERR_DTYPE: return "AAL_ERR_DTYPE: unsupported element type";
@@ -182,13 +193,18 @@ const char* aal_status_string(aal_status_t status) {
 
 const char* aal_last_error(void) { return g_last_error; }
 
-aal_status_t aal_eal_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N,
-                                int32_t K, int32_t V, float temp_draft, float* loss, float* eal_per_window,
-                                float* accept, int32_t* target_argmax, void* grad_draft, aal_dtype_t grad_dtype,
-                                const float* grad_scale, uint32_t flags, void* workspace, size_t workspace_bytes,
-                                hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The bodies of the EAL, WTV and simulation entry points, with the element
+// types as the integers the caller passed.
+aal_status_t eal_impl(const void* z_draft, const void* z_target, int in_dtype, int64_t N, int32_t K, int32_t V,
+                      float temp_draft, float* loss, float* eal_per_window, float* accept, int32_t* target_argmax,
+                      void* grad_draft, int grad_dtype, const float* grad_scale, uint32_t flags, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream) {
   clear_error();
-  const CommonIn c{z_draft, z_target, int(in_dtype), N, K, V, loss, grad_draft, int(grad_dtype),
+  const CommonIn c{z_draft, z_target, raw(in_dtype), N, K, V, loss, grad_draft, raw(grad_dtype),
                    workspace, workspace_bytes};
   aal_status_t s = validate_common(c);
   if (s != AAL_OK) return s;
@@ -198,8 +214,8 @@ aal_status_t aal_eal_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_d
   if (flags & ~AAL_FLAG_STREAMING) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
   aal::LossArgs a{};
   a.mode = aal::Mode::kEal;
-  a.in = to_dtype(in_dtype);
-  a.gd = to_dtype(grad_dtype);
+  a.in = to_dtype(raw(in_dtype));
+  a.gd = to_dtype(raw(grad_dtype));
   a.zd = z_draft;
   a.zt = z_target;
   a.N = N;
@@ -219,13 +235,12 @@ aal_status_t aal_eal_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_d
   return run_loss(a, flags);
 }
 
-aal_status_t aal_wtv_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N,
-                                int32_t K, int32_t V, float temp_draft, float temp_target, float* loss,
-                                float* eal_per_window, float* accept, void* grad_draft, aal_dtype_t grad_dtype,
-                                const float* grad_scale, uint32_t flags, void* workspace, size_t workspace_bytes,
-                                hipStream_t stream) {
+aal_status_t wtv_impl(const void* z_draft, const void* z_target, int in_dtype, int64_t N, int32_t K, int32_t V,
+                      float temp_draft, float temp_target, float* loss, float* eal_per_window, float* accept,
+                      void* grad_draft, int grad_dtype, const float* grad_scale, uint32_t flags, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream) {
   clear_error();
-  const CommonIn c{z_draft, z_target, int(in_dtype), N, K, V, loss, grad_draft, int(grad_dtype),
+  const CommonIn c{z_draft, z_target, raw(in_dtype), N, K, V, loss, grad_draft, raw(grad_dtype),
                    workspace, workspace_bytes};
   aal_status_t s = validate_common(c);
   if (s != AAL_OK) return s;
@@ -238,8 +253,8 @@ aal_status_t aal_wtv_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_d
   if (flags & ~AAL_FLAG_STREAMING) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
   aal::LossArgs a{};
   a.mode = aal::Mode::kWtv;
-  a.in = to_dtype(in_dtype);
-  a.gd = to_dtype(grad_dtype);
+  a.in = to_dtype(raw(in_dtype));
+  a.gd = to_dtype(raw(grad_dtype));
   a.zd = z_draft;
   a.zt = z_target;
   a.N = N;
@@ -259,11 +274,10 @@ aal_status_t aal_wtv_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_d
   return run_loss(a, flags);
 }
 
-aal_status_t aal_sim_accept_grpo_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int32_t P,
-                                    int32_t G, int32_t K, int32_t V, float temperature, const float* u1,
-                                    const float* u2, int32_t* draft_token, int32_t* accept, int32_t* reward,
-                                    float* advantage, float eps, int32_t std_ddof, float adv_clip, void* workspace,
-                                    size_t workspace_bytes, hipStream_t stream) {
+aal_status_t sim_impl(const void* z_draft, const void* z_target, int in_dtype, int32_t P, int32_t G, int32_t K,
+                      int32_t V, float temperature, const float* u1, const float* u2, int32_t* draft_token,
+                      int32_t* accept, int32_t* reward, float* advantage, float eps, int32_t std_ddof,
+                      float adv_clip, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   clear_error();
   if (!z_draft || !z_target || !u1 || !u2) return fail(AAL_ERR_ARG, "z_draft, z_target, u1, u2 must be non-NULL");
   if (!reward || !advantage) return fail(AAL_ERR_ARG, "reward and advantage must be non-NULL");
@@ -272,7 +286,7 @@ aal_status_t aal_sim_accept_grpo_ex(const void* z_draft, const void* z_target, a
   if (std_ddof < 0 || G <= std_ddof) return fail(AAL_ERR_ARG, "need 0 <= std_ddof < G");
   const int64_t rows = int64_t(P) * G * K;
   if (rows >= (int64_t(1) << 31)) return fail(AAL_ERR_ARG, "P*G*K must be < 2^31");
-  if (!valid_dtype(int(in_dtype))) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", int(in_dtype));
+  if (!valid_dtype(raw(in_dtype))) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", raw(in_dtype));
   const float sc = scale_for(temperature);
   if (!positive_finite(temperature) || sc == 0.f)
     return fail(AAL_ERR_ARG, "temperature must be finite, > 0 and >= 1e-37");
@@ -287,7 +301,7 @@ aal_status_t aal_sim_accept_grpo_ex(const void* z_draft, const void* z_target, a
   aal::Workspace ws = aal::carve(workspace, rows, int64_t(P) * G);
   int32_t* scratch = reinterpret_cast<int32_t*>(ws.stats);  // rows * 32 bytes >= 2 int32 per row
   aal::SimArgs a{};
-  a.in = to_dtype(in_dtype);
+  a.in = to_dtype(raw(in_dtype));
   a.zd = z_draft;
   a.zt = z_target;
   a.P = P;
@@ -310,20 +324,51 @@ aal_status_t aal_sim_accept_grpo_ex(const void* z_draft, const void* z_target, a
   return AAL_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+aal_status_t aal_eal_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N,
+                                int32_t K, int32_t V, float temp_draft, float* loss, float* eal_per_window,
+                                float* accept, int32_t* target_argmax, void* grad_draft, aal_dtype_t grad_dtype,
+                                const float* grad_scale, uint32_t flags, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  return eal_impl(z_draft, z_target, raw(in_dtype), N, K, V, temp_draft, loss, eal_per_window, accept, target_argmax,
+                  grad_draft, raw(grad_dtype), grad_scale, flags, workspace, workspace_bytes, stream);
+}
+
 aal_status_t aal_eal_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N, int32_t K,
                              int32_t V, float temp_draft, float* loss, float* eal_per_window, float* accept,
                              int32_t* target_argmax, void* grad_draft, aal_dtype_t grad_dtype,
                              const float* grad_scale, void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  return aal_eal_fwd_bwd_ex(z_draft, z_target, in_dtype, N, K, V, temp_draft, loss, eal_per_window, accept,
-                            target_argmax, grad_draft, grad_dtype, grad_scale, 0u, workspace, workspace_bytes, stream);
+  return eal_impl(z_draft, z_target, raw(in_dtype), N, K, V, temp_draft, loss, eal_per_window, accept, target_argmax,
+                  grad_draft, raw(grad_dtype), grad_scale, 0u, workspace, workspace_bytes, stream);
+}
+
+aal_status_t aal_wtv_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N,
+                                int32_t K, int32_t V, float temp_draft, float temp_target, float* loss,
+                                float* eal_per_window, float* accept, void* grad_draft, aal_dtype_t grad_dtype,
+                                const float* grad_scale, uint32_t flags, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  return wtv_impl(z_draft, z_target, raw(in_dtype), N, K, V, temp_draft, temp_target, loss, eal_per_window, accept,
+                  grad_draft, raw(grad_dtype), grad_scale, flags, workspace, workspace_bytes, stream);
+}
+
+aal_status_t aal_sim_accept_grpo_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int32_t P,
+                                    int32_t G, int32_t K, int32_t V, float temperature, const float* u1,
+                                    const float* u2, int32_t* draft_token, int32_t* accept, int32_t* reward,
+                                    float* advantage, float eps, int32_t std_ddof, float adv_clip, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream) {
+  return sim_impl(z_draft, z_target, raw(in_dtype), P, G, K, V, temperature, u1, u2, draft_token, accept, reward,
+                  advantage, eps, std_ddof, adv_clip, workspace, workspace_bytes, stream);
 }
 
 aal_status_t aal_wtv_fwd_bwd(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N, int32_t K,
                              int32_t V, float temp_draft, float temp_target, float* loss, float* eal_per_window,
                              float* accept, void* grad_draft, aal_dtype_t grad_dtype, const float* grad_scale,
                              void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  return aal_wtv_fwd_bwd_ex(z_draft, z_target, in_dtype, N, K, V, temp_draft, temp_target, loss, eal_per_window,
-                            accept, grad_draft, grad_dtype, grad_scale, 0u, workspace, workspace_bytes, stream);
+  return wtv_impl(z_draft, z_target, raw(in_dtype), N, K, V, temp_draft, temp_target, loss, eal_per_window, accept,
+                  grad_draft, raw(grad_dtype), grad_scale, 0u, workspace, workspace_bytes, stream);
 }
 
 aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int32_t P,
@@ -331,8 +376,8 @@ aal_status_t aal_sim_accept_grpo(const void* z_draft, const void* z_target, aal_
                                  const float* u2, int32_t* draft_token, int32_t* reward, float* advantage, float eps,
                                  int32_t std_ddof, float adv_clip, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream) {
-  return aal_sim_accept_grpo_ex(z_draft, z_target, in_dtype, P, G, K, V, temperature, u1, u2, draft_token, nullptr,
-                                reward, advantage, eps, std_ddof, adv_clip, workspace, workspace_bytes, stream);
+  return sim_impl(z_draft, z_target, raw(in_dtype), P, G, K, V, temperature, u1, u2, draft_token, nullptr, reward,
+                  advantage, eps, std_ddof, adv_clip, workspace, workspace_bytes, stream);
 }
 
 aal_status_t aal_wtv_fwd_bwd_noalloc(const void* z_draft, const void* z_target, aal_dtype_t in_dtype, int64_t N,
@@ -352,16 +397,15 @@ aal_status_t aal_wtv_fwd_bwd_noalloc(const void* z_draft, const void* z_target, 
   void* ws = nullptr;
   const aal_status_t st = scratch_for_current_device(&ws);
   if (st != AAL_OK) return st;
-  return aal_wtv_fwd_bwd_ex(z_draft, z_target, in_dtype, N, K, V, temp_draft, temp_target, loss, eal_per_window,
-                            accept, grad_draft, grad_dtype, grad_scale, 0u, ws, size_t(AAL_NOALLOC_SCRATCH_BYTES),
-                            stream);
+  return wtv_impl(z_draft, z_target, raw(in_dtype), N, K, V, temp_draft, temp_target, loss, eal_per_window, accept,
+                  grad_draft, raw(grad_dtype), grad_scale, 0u, ws, size_t(AAL_NOALLOC_SCRATCH_BYTES), stream);
 }
 
 size_t aal_loss_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32_t K) {
-  if (B < 1 || K < 1 || (layout == AAL_LAYOUT_SEQUENCES && S < 1)) return 0;
-  if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES) return 0;
-  const int64_t rows = layout == AAL_LAYOUT_WINDOWS ? B * K : B * S;
-  const int64_t windows = layout == AAL_LAYOUT_WINDOWS ? B : B * int64_t(S >= K ? S - K + 1 : 0);
+  if (B < 1 || K < 1 || (raw(layout) == AAL_LAYOUT_SEQUENCES && S < 1)) return 0;
+  if (raw(layout) != AAL_LAYOUT_WINDOWS && raw(layout) != AAL_LAYOUT_SEQUENCES) return 0;
+  const int64_t rows = raw(layout) == AAL_LAYOUT_WINDOWS ? B * K : B * S;
+  const int64_t windows = raw(layout) == AAL_LAYOUT_WINDOWS ? B : B * int64_t(S >= K ? S - K + 1 : 0);
   return aal::general_workspace_bytes(rows, windows);
 }
 
@@ -372,17 +416,17 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
                               aal_dtype_t grad_dtype, const float* grad_scale, uint32_t flags, void* workspace,
                               size_t workspace_bytes, hipStream_t stream) {
   clear_error();
-  if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES)
-    return fail(AAL_ERR_ARG, "unknown layout %d", int(layout));
+  if (raw(layout) != AAL_LAYOUT_WINDOWS && raw(layout) != AAL_LAYOUT_SEQUENCES)
+    return fail(AAL_ERR_ARG, "unknown layout %d", raw(layout));
   if (B < 1) return fail(AAL_ERR_ARG, "B must be >= 1 (got %lld)", (long long)B);
   if (K < 1 || K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", K);
   if (V < 1) return fail(AAL_ERR_ARG, "V must be >= 1 (got %d)", V);
-  if (layout == AAL_LAYOUT_SEQUENCES && S < 1) return fail(AAL_ERR_ARG, "S must be >= 1 (got %d)", S);
-  const int64_t per = layout == AAL_LAYOUT_WINDOWS ? K : S;
+  if (raw(layout) == AAL_LAYOUT_SEQUENCES && S < 1) return fail(AAL_ERR_ARG, "S must be >= 1 (got %d)", S);
+  const int64_t per = raw(layout) == AAL_LAYOUT_WINDOWS ? K : S;
   if (B > ((int64_t(1) << 31) - 1) / per) return fail(AAL_ERR_ARG, "the number of rows must be < 2^31");
   const int64_t R = B * per;
   if (R > (int64_t(1) << 62) / V) return fail(AAL_ERR_ARG, "rows*V must be < 2^62");
-  const int64_t W = layout == AAL_LAYOUT_WINDOWS ? B : B * int64_t(S >= K ? S - K + 1 : 0);
+  const int64_t W = raw(layout) == AAL_LAYOUT_WINDOWS ? B : B * int64_t(S >= K ? S - K + 1 : 0);
   auto finite = [](float x) {
     uint32_t u;
     memcpy(&u, &x, sizeof u);
@@ -397,8 +441,8 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
   if (need_t && !z_target)
     return fail(AAL_ERR_ARG, "z_target must be non-NULL unless only the EAL term is asked for with labels");
   if (!loss) return fail(AAL_ERR_ARG, "loss must be non-NULL");
-  if (!valid_dtype(int(in_dtype))) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", int(in_dtype));
-  if (grad_draft && !valid_dtype(int(grad_dtype))) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", int(grad_dtype));
+  if (!valid_dtype(raw(in_dtype))) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", raw(in_dtype));
+  if (grad_draft && !valid_dtype(raw(grad_dtype))) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", raw(grad_dtype));
   if (!aligned(z_draft, 16) || (z_target && !aligned(z_target, 16)))
     return fail(AAL_ERR_ALIGN, "logit pointers must be 16-byte aligned");
   if (grad_draft && !aligned(grad_draft, 16)) return fail(AAL_ERR_ALIGN, "grad_draft must be 16-byte aligned");
@@ -415,14 +459,14 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
     return fail(AAL_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
   uint8_t* wp = static_cast<uint8_t*>(workspace);
   aal::GenArgs a{};
-  a.in = to_dtype(in_dtype);
-  a.gd = to_dtype(grad_dtype);
+  a.in = to_dtype(raw(in_dtype));
+  a.gd = to_dtype(raw(grad_dtype));
   a.zd = z_draft;
   a.zt = need_t ? z_target : nullptr;
   a.labels = labels;
-  a.layout = int(layout);
+  a.layout = raw(layout);
   a.B = B;
-  a.S = layout == AAL_LAYOUT_WINDOWS ? K : S;
+  a.S = raw(layout) == AAL_LAYOUT_WINDOWS ? K : S;
   a.K = K;
   a.V = V;
   a.R = R;
@@ -466,10 +510,10 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
 
 size_t aal_grpo_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32_t G, int32_t m, int32_t K) {
   if (B < 1 || K < 1 || m < 1) return 0;
-  if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES) return 0;
-  if (layout == AAL_LAYOUT_SEQUENCES && (G < 1 || S < 1)) return 0;
-  const int64_t groups = layout == AAL_LAYOUT_WINDOWS ? B : B * G;
-  const int64_t rows = layout == AAL_LAYOUT_WINDOWS ? B * m * K : B * S;
+  if (raw(layout) != AAL_LAYOUT_WINDOWS && raw(layout) != AAL_LAYOUT_SEQUENCES) return 0;
+  if (raw(layout) == AAL_LAYOUT_SEQUENCES && (G < 1 || S < 1)) return 0;
+  const int64_t groups = raw(layout) == AAL_LAYOUT_WINDOWS ? B : B * G;
+  const int64_t rows = raw(layout) == AAL_LAYOUT_WINDOWS ? B * m * K : B * S;
   return aal::grpo_workspace_bytes(rows, groups, groups * m);
 }
 
@@ -480,13 +524,13 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
                               float* advantage, float* log_rho, void* grad_theta, aal_dtype_t grad_dtype,
                               const float* grad_scale, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   clear_error();
-  if (layout != AAL_LAYOUT_WINDOWS && layout != AAL_LAYOUT_SEQUENCES)
-    return fail(AAL_ERR_ARG, "unknown layout %d", int(layout));
+  if (raw(layout) != AAL_LAYOUT_WINDOWS && raw(layout) != AAL_LAYOUT_SEQUENCES)
+    return fail(AAL_ERR_ARG, "unknown layout %d", raw(layout));
   if (B < 1) return fail(AAL_ERR_ARG, "B must be >= 1 (got %lld)", (long long)B);
   if (K < 1 || K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", K);
   if (m < 1 || m > 64) return fail(AAL_ERR_ARG, "m must be in [1, 64] (got %d)", m);
   if (V < 1) return fail(AAL_ERR_ARG, "V must be >= 1 (got %d)", V);
-  const bool seq = layout == AAL_LAYOUT_SEQUENCES;
+  const bool seq = raw(layout) == AAL_LAYOUT_SEQUENCES;
   if (seq) {
     if (G < 1) return fail(AAL_ERR_ARG, "G must be >= 1 (got %d)", G);
     if (S < m + K - 1) return fail(AAL_ERR_ARG, "S must be >= m + K - 1 (got S=%d, m=%d, K=%d)", S, m, K);
@@ -501,8 +545,8 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
   if (!z_theta || !z_ref) return fail(AAL_ERR_ARG, "z_theta and z_ref must be non-NULL");
   if (!z_target && !labels) return fail(AAL_ERR_ARG, "z_target or labels must be given");
   if (!loss) return fail(AAL_ERR_ARG, "loss must be non-NULL");
-  if (!valid_dtype(int(in_dtype))) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", int(in_dtype));
-  if (grad_theta && !valid_dtype(int(grad_dtype))) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", int(grad_dtype));
+  if (!valid_dtype(raw(in_dtype))) return fail(AAL_ERR_DTYPE, "unknown in_dtype %d", raw(in_dtype));
+  if (grad_theta && !valid_dtype(raw(grad_dtype))) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", raw(grad_dtype));
   if (!aligned(z_theta, 16) || !aligned(z_ref, 16) || (z_target && !aligned(z_target, 16)))
     return fail(AAL_ERR_ALIGN, "logit pointers must be 16-byte aligned");
   if (grad_theta && !aligned(grad_theta, 16)) return fail(AAL_ERR_ALIGN, "grad_theta must be 16-byte aligned");
@@ -533,13 +577,13 @@ aal_status_t aal_grpo_fwd_bwd(const void* z_theta, const void* z_ref, const void
     return fail(AAL_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
   uint8_t* wp = static_cast<uint8_t*>(workspace);
   aal::GrpoArgs a{};
-  a.in = to_dtype(in_dtype);
-  a.gd = to_dtype(grad_dtype);
+  a.in = to_dtype(raw(in_dtype));
+  a.gd = to_dtype(raw(grad_dtype));
   a.zth = z_theta;
   a.zrf = z_ref;
   a.zt = labels ? nullptr : z_target;
   a.labels = labels;
-  a.layout = int(layout);
+  a.layout = raw(layout);
   a.B = B;
   a.S = seq ? S : m * K;
   a.G = seq ? G : 1;
@@ -580,10 +624,10 @@ aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, cons
                                  aal_vp_mode_t mode, float temp_draft, float temp_target, aal_vp_part_t* parts,
                                  hipStream_t stream) {
   clear_error();
-  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
-  if (labels && mode != AAL_VP_EAL) return fail(AAL_ERR_ARG, "labels are for EAL mode only");
+  if (!valid_vp_mode(raw(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", raw(mode));
+  if (labels && raw(mode) != AAL_VP_EAL) return fail(AAL_ERR_ARG, "labels are for EAL mode only");
   if (labels && !aligned(labels, 4)) return fail(AAL_ERR_ALIGN, "labels must be 4-byte aligned");
-  aal_status_t st = validate_vp_slice(z_draft, labels ? nullptr : z_target, !labels, int(in_dtype), rows, V_slice,
+  aal_status_t st = validate_vp_slice(z_draft, labels ? nullptr : z_target, !labels, raw(in_dtype), rows, V_slice,
                                       v0);
   if (st != AAL_OK) return st;
   if (V_total < 1 || int64_t(v0) + V_slice > V_total)
@@ -592,16 +636,16 @@ aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, cons
   if (!parts) return fail(AAL_ERR_ARG, "parts must be non-NULL");
   if (!aligned(parts, 4)) return fail(AAL_ERR_ALIGN, "parts must be 4-byte aligned");
   aal::VpSlice s{};
-  if ((st = vp_scales(int(mode), temp_draft, temp_target, &s.scd, &s.sct)) != AAL_OK) return st;
+  if ((st = vp_scales(raw(mode), temp_draft, temp_target, &s.scd, &s.sct)) != AAL_OK) return st;
   s.zd = z_draft;
   s.zt = labels ? nullptr : z_target;
   s.labels = labels;
-  s.in = to_dtype(in_dtype);
+  s.in = to_dtype(raw(in_dtype));
   s.rows = rows;
   s.vs = V_slice;
   s.v0 = v0;
   s.vtot = V_total;
-  s.mode = vp_mode(int(mode));
+  s.mode = vp_mode(raw(mode));
   s.stream = stream;
   const hipError_t e = aal::launch_vp_partials(s, parts);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -611,17 +655,17 @@ aal_status_t aal_vp_row_partials(const void* z_draft, const void* z_target, cons
 aal_status_t aal_vp_merge_rows(const aal_vp_part_t* parts_all, int32_t R, int64_t rows, aal_vp_mode_t mode,
                                float temp_draft, float temp_target, aal_vp_row_t* row, hipStream_t stream) {
   clear_error();
-  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
+  if (!valid_vp_mode(raw(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", raw(mode));
   if (!parts_all || !row) return fail(AAL_ERR_ARG, "parts_all and row must be non-NULL");
   if (R < 1) return fail(AAL_ERR_ARG, "R must be >= 1 (got %d)", R);
   if (rows < 1) return fail(AAL_ERR_ARG, "rows must be >= 1 (got %lld)", (long long)rows);
   if (rows > (int64_t(1) << 56) / R) return fail(AAL_ERR_ARG, "R*rows must be < 2^56");
   if (!aligned(parts_all, 4) || !aligned(row, 4)) return fail(AAL_ERR_ALIGN, "records must be 4-byte aligned");
   float scd, sct;
-  aal_status_t st = vp_scales(int(mode), temp_draft, temp_target, &scd, &sct);
+  aal_status_t st = vp_scales(raw(mode), temp_draft, temp_target, &scd, &sct);
   if (st != AAL_OK) return st;
   const hipError_t e =
-      aal::launch_vp_merge(parts_all, R, rows, vp_mode(int(mode)), scd, sct, row, stream);
+      aal::launch_vp_merge(parts_all, R, rows, vp_mode(raw(mode)), scd, sct, row, stream);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
 }
@@ -630,7 +674,7 @@ aal_status_t aal_vp_accept_partials(const void* z_draft, const void* z_target, a
                                     int32_t V_slice, float temp_draft, float temp_target, const aal_vp_row_t* row,
                                     aal_vp_acc_t* acc, hipStream_t stream) {
   clear_error();
-  aal_status_t st = validate_vp_slice(z_draft, z_target, true, int(in_dtype), rows, V_slice, 0);
+  aal_status_t st = validate_vp_slice(z_draft, z_target, true, raw(in_dtype), rows, V_slice, 0);
   if (st != AAL_OK) return st;
   if (!row || !acc) return fail(AAL_ERR_ARG, "row and acc must be non-NULL");
   if (!aligned(row, 4) || !aligned(acc, 4)) return fail(AAL_ERR_ALIGN, "records must be 4-byte aligned");
@@ -638,7 +682,7 @@ aal_status_t aal_vp_accept_partials(const void* z_draft, const void* z_target, a
   if ((st = vp_scales(AAL_VP_WTV, temp_draft, temp_target, &s.scd, &s.sct)) != AAL_OK) return st;
   s.zd = z_draft;
   s.zt = z_target;
-  s.in = to_dtype(in_dtype);
+  s.in = to_dtype(raw(in_dtype));
   s.rows = rows;
   s.vs = V_slice;
   s.v0 = 0;
@@ -653,12 +697,12 @@ aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, 
                                 aal_vp_mode_t mode, float temp_draft, const float* grad_scale, float* loss,
                                 float* eal_per_window, float* accept, int32_t* target_argmax, hipStream_t stream) {
   clear_error();
-  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
+  if (!valid_vp_mode(raw(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", raw(mode));
   if (!row || !loss || !eal_per_window) return fail(AAL_ERR_ARG, "row, loss and eal_per_window must be non-NULL");
   if (N < 1) return fail(AAL_ERR_ARG, "N must be >= 1 (got %lld)", (long long)N);
   if (K < 1 || K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", K);
   if (N > (int64_t(1) << 31) / K) return fail(AAL_ERR_ARG, "N*K must be < 2^31");
-  const bool wtv = mode == AAL_VP_WTV;
+  const bool wtv = raw(mode) == AAL_VP_WTV;
   if (wtv && !acc_all) return fail(AAL_ERR_ARG, "acc_all must be non-NULL in WTV mode");
   if (wtv && R < 1) return fail(AAL_ERR_ARG, "R must be >= 1 (got %d)", R);
   if (wtv && N * K > (int64_t(1) << 56) / R) return fail(AAL_ERR_ARG, "R*N*K must be < 2^56");
@@ -666,7 +710,7 @@ aal_status_t aal_vp_window_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all, 
   float scd, sct;
   aal_status_t st = vp_scales(AAL_VP_EAL, temp_draft, 1.f, &scd, &sct);
   if (st != AAL_OK) return st;
-  const hipError_t e = aal::launch_vp_scan(row, wtv ? acc_all : nullptr, wtv ? R : 0, N, K, vp_mode(int(mode)),
+  const hipError_t e = aal::launch_vp_scan(row, wtv ? acc_all : nullptr, wtv ? R : 0, N, K, vp_mode(raw(mode)),
                                            1.0f / temp_draft, grad_scale, loss, eal_per_window, accept,
                                            wtv ? nullptr : target_argmax, stream);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -678,13 +722,13 @@ aal_status_t aal_vp_sequence_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all
                                   float* loss, float* eal_per_window, float* accept, int32_t* target_argmax,
                                   hipStream_t stream) {
   clear_error();
-  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
+  if (!valid_vp_mode(raw(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", raw(mode));
   if (!row || !loss || !eal_per_window) return fail(AAL_ERR_ARG, "row, loss and eal_per_window must be non-NULL");
   if (B < 1) return fail(AAL_ERR_ARG, "B must be >= 1 (got %lld)", (long long)B);
   if (K < 1 || K > 64) return fail(AAL_ERR_ARG, "K must be in [1, 64] (got %d)", K);
   if (S < K) return fail(AAL_ERR_ARG, "S must be >= K (got S = %d, K = %d)", S, K);
   if (B > (int64_t(1) << 31) / S) return fail(AAL_ERR_ARG, "B*S must be < 2^31");
-  const bool wtv = mode == AAL_VP_WTV;
+  const bool wtv = raw(mode) == AAL_VP_WTV;
   if (wtv && !acc_all) return fail(AAL_ERR_ARG, "acc_all must be non-NULL in WTV mode");
   if (wtv && R < 1) return fail(AAL_ERR_ARG, "R must be >= 1 (got %d)", R);
   if (wtv && B * S > (int64_t(1) << 56) / R) return fail(AAL_ERR_ARG, "R*B*S must be < 2^56");
@@ -693,7 +737,7 @@ aal_status_t aal_vp_sequence_scan(aal_vp_row_t* row, const aal_vp_acc_t* acc_all
   aal_status_t st = vp_scales(AAL_VP_EAL, temp_draft, 1.f, &scd, &sct);
   if (st != AAL_OK) return st;
   const hipError_t e = aal::launch_vp_seq_scan(row, wtv ? acc_all : nullptr, wtv ? R : 0, B, S, K,
-                                               vp_mode(int(mode)), 1.0f / temp_draft, grad_scale, loss,
+                                               vp_mode(raw(mode)), 1.0f / temp_draft, grad_scale, loss,
                                                eal_per_window, accept, wtv ? nullptr : target_argmax,
                                                stream);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -704,25 +748,25 @@ aal_status_t aal_vp_grad(const void* z_draft, const void* z_target, aal_dtype_t 
                          int32_t V_slice, int32_t v0, aal_vp_mode_t mode, float temp_draft, float temp_target,
                          const aal_vp_row_t* row, void* grad_draft, aal_dtype_t grad_dtype, hipStream_t stream) {
   clear_error();
-  if (!valid_vp_mode(int(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", int(mode));
+  if (!valid_vp_mode(raw(mode))) return fail(AAL_ERR_ARG, "unknown mode %d", raw(mode));
   aal_status_t st =
-      validate_vp_slice(z_draft, z_target, mode == AAL_VP_WTV, int(in_dtype), rows, V_slice, v0);
+      validate_vp_slice(z_draft, z_target, raw(mode) == AAL_VP_WTV, raw(in_dtype), rows, V_slice, v0);
   if (st != AAL_OK) return st;
   if (!row || !grad_draft) return fail(AAL_ERR_ARG, "row and grad_draft must be non-NULL");
-  if (!valid_dtype(int(grad_dtype))) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", int(grad_dtype));
+  if (!valid_dtype(raw(grad_dtype))) return fail(AAL_ERR_DTYPE, "unknown grad_dtype %d", raw(grad_dtype));
   if (!aligned(row, 4)) return fail(AAL_ERR_ALIGN, "records must be 4-byte aligned");
   if (!aligned(grad_draft, 16)) return fail(AAL_ERR_ALIGN, "grad_draft must be 16-byte aligned");
   aal::VpSlice s{};
-  if ((st = vp_scales(int(mode), temp_draft, temp_target, &s.scd, &s.sct)) != AAL_OK) return st;
+  if ((st = vp_scales(raw(mode), temp_draft, temp_target, &s.scd, &s.sct)) != AAL_OK) return st;
   s.zd = z_draft;
-  s.zt = mode == AAL_VP_WTV ? z_target : nullptr;
-  s.in = to_dtype(in_dtype);
+  s.zt = raw(mode) == AAL_VP_WTV ? z_target : nullptr;
+  s.in = to_dtype(raw(in_dtype));
   s.rows = rows;
   s.vs = V_slice;
   s.v0 = v0;
-  s.mode = vp_mode(int(mode));
+  s.mode = vp_mode(raw(mode));
   s.stream = stream;
-  const hipError_t e = aal::launch_vp_grad(s, row, grad_draft, to_dtype(grad_dtype));
+  const hipError_t e = aal::launch_vp_grad(s, row, grad_draft, to_dtype(raw(grad_dtype)));
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return AAL_OK;
 }
