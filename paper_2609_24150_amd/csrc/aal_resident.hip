@@ -252,24 +252,14 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           m1[k] = mt == kNegInf ? kNegInf : mtsc;
           s1[k] = st;
         } else {
-          float best = kNegInf, bz = kNegInf;
-          int bidx = INT_MAX;
+          float best = kNegInf, bi, bz;
 #pragma unroll
-          for (int v = 0; v < NV; ++v) {
-            float xd[E];  // the draft logits again, for the payload (not kept from above)
-            pin(rd[k][v]);
-            unpackv<TI, E>(rd[k][v], xd);
+          for (int v = 0; v < NV; ++v)
 #pragma unroll
-            for (int e = 0; e < E; ++e)
-              if (xs[v][e] > best) {
-                best = xs[v][e];
-                bidx = col[v] * E + e;
-                bz = xd[e];
-              }
-          }
+            for (int e = 0; e < E; ++e) best = fmaxf(best, xs[v][e]);
+          first_max<TI, NV, E, kBlock>(xs, rd[k], best, col[0] * E, bi, bz);
           // reduced over the wave right away: the results are wave-uniform, so
           // the per-lane payloads are short-lived
-          float bi = __builtin_bit_cast(float, bidx);
           wave_argmax(best, bi, bz);
           m1[k] = best;
           s1[k] = bi;

@@ -149,6 +149,55 @@ __device__ __forceinline__ void argmax_fold(float& bv, float& bi, float& bz, flo
   }
 }
 
+// log2 p - log2 q for the KL term's p (log p - log q), finite wherever p = 0
+// (t = -inf, where the difference is -inf, or undefined when q = 0 too): one
+// max instead of a test of p, since 0 times the lowest finite float is 0,
+// the limit of p log p.  Where q = 0 < p the difference stays +inf (KL is
+// infinite).  On NaN operands the hardware max returns the other operand.
+__device__ __forceinline__ float kl_diff(float t, float u) { return fmaxf(t - u, -3.402823466e38f); }
+
+// A thread's part of the greedy token of one row: the lowest column among its
+// elements that holds m, the maximum of those elements, with the draft logit
+// at that column as the payload.  xs are the row's target logits as
+// unpacked from its NV vectors, dw the row's packed draft vectors; element e
+// of vector v sits in column base + v * kBlock * E + e.  With the maximum
+// known beforehand (the normaliser needs it anyway) a compare and a select
+// per element suffice, and the payload is chosen as the packed draft word of
+// the matching pair (one select per word) and unpacked once at the end.
+// m = -inf (no finite element) gives index INT_MAX and payload -inf, as
+// a strict running comparison against -inf would.
+template <class TI, int NV, int E, int kBlock>
+__device__ __forceinline__ void first_max(const float (&xs)[NV][E], const u32x4 (&dw)[NV], float m, int base,
+                                          float& bidx, float& bz) {
+  constexpr int EPW = E / 4;  // elements per 32-bit word: 2 (bf16) or 1 (fp32)
+  int li = 0;
+  uint32_t w = 0;
+#pragma unroll
+  for (int v = NV - 1; v >= 0; --v)
+#pragma unroll
+    for (int q = 3; q >= 0; --q) {
+      bool hit = false;
+#pragma unroll
+      for (int h = EPW - 1; h >= 0; --h) {
+        const int e = q * EPW + h;
+        if (xs[v][e] == m) {
+          li = v * E + e;  // an inline constant; the column is formed once below
+          hit = true;
+        }
+      }
+      if (hit) w = dw[v][q];
+    }
+  float z;
+  if constexpr (EPW == 2) {
+    z = __builtin_bit_cast(float, (li & 1) ? (w & 0xffff0000u) : (w << 16));
+  } else {
+    z = __builtin_bit_cast(float, w);
+  }
+  const bool none = m == kNegInf;
+  bidx = __builtin_bit_cast(float, none ? INT_MAX : base + (li / E) * (kBlock * E) + li % E);
+  bz = none ? kNegInf : z;
+}
+
 // Wave-wide argmax of (value, index) pairs, lowest index on ties, with the
 // payload of the winning lane.  All lanes receive the result.
 __device__ __forceinline__ void wave_argmax(float& bv, float& bi, float& bz) {

@@ -286,12 +286,14 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
         m1[k] = kNegInf;
         s1[k] = 0.f;
-        if constexpr (PQ) {
-          float mt = kNegInf;
+        float mt = kNegInf;  // the target's maximum (normaliser and greedy token)
+        if constexpr (PQ || AM) {
 #pragma unroll
           for (int v = 0; v < NV; ++v)
 #pragma unroll
             for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+        }
+        if constexpr (PQ) {
           const float mtsc = mt * p.sct;
           float st = 0.f;
           if (mt != kNegInf) {
@@ -304,22 +306,8 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           s1[k] = st;
         }
         if constexpr (AM) {
-          float best = kNegInf, bz = kNegInf;
-          int bidx = INT_MAX;
-#pragma unroll
-          for (int v = 0; v < NV; ++v) {
-            float xd[E];
-            pin(rd[k][v]);
-            unpackv<TI, E>(rd[k][v], xd);
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-              if (xs[v][e] > best) {
-                best = xs[v][e];
-                bidx = col[v] * E + e;
-                bz = xd[e];
-              }
-          }
-          float bi = __builtin_bit_cast(float, bidx);
+          float best = mt, bi, bz;
+          first_max<TI, NV, E, kBlock>(xs, rd[k], mt, col[0] * E, bi, bz);
           wave_argmax(best, bi, bz);
           // wave-uniform from here: stored right away rather than kept live
           if (lane == 0) {
@@ -514,7 +502,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
             }
             if constexpr (KL) {
               const float ep = ex2(t);  // p 2^l2s_d; p = 0 contributes nothing
-              sk = __builtin_fmaf(ep, (ep > 0.f) ? (t - u) : 0.f, sk);
+              sk = __builtin_fmaf(ep, kl_diff(t, u), sk);
             }
           }
         }
@@ -772,7 +760,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           if constexpr (KL) {
             const float ep = ex2(t);  // p 2^l2s_d; p = 0 contributes nothing
             g[e] = __builtin_fmaf(cP, ep, g[e]);
-            if constexpr (KLC) klp[k] = __builtin_fmaf(ep, ep > 0.f ? t - u : 0.f, klp[k]);
+            if constexpr (KLC) klp[k] = __builtin_fmaf(ep, kl_diff(t, u), klp[k]);
           }
         }
       } else {
