@@ -645,22 +645,28 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       float dt = 0.f, de = 0.f;
       if (k < nvalid && t >= 0 && t <= p.S - K) {
         const int o0 = K + (t - j * K);  // the window's first row in sh_a
+        // The window's acceptances are read up front and the recurrences are
+        // straight-line: a factor outside the product enters as 1.0 and a step
+        // outside the nesting keeps the previous value, which gives the same
+        // bits as skipping them (a branch per factor made this one-wave step
+        // wait for each LDS read in turn, with every other wave at the barrier).
+        float xa[K], xe[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+          xa[i] = sh_a[o0 + i][0];
+          xe[i] = sh_a[o0 + i][1];
+        }
         double ptv = 1.0, peal = 1.0, stv = 1.0, seal = 1.0, etv = 0.0, eeal = 0.0;
 #pragma unroll
         for (int i = 0; i < K; ++i) {
-          const double xa = double(sh_a[o0 + i][0]), xe = double(sh_a[o0 + i][1]);
-          if (i < jj) {
-            ptv *= xa;
-            peal *= xe;
-          }
+          ptv *= i < jj ? double(xa[i]) : 1.0;
+          peal *= i < jj ? double(xe[i]) : 1.0;
         }
 #pragma unroll
         for (int i = K - 1; i > 0; --i) {
-          const double xa = double(sh_a[o0 + i][0]), xe = double(sh_a[o0 + i][1]);
-          if (i > jj) {
-            stv = 1.0 + xa * stv;
-            seal = 1.0 + xe * seal;
-          }
+          const double nt = 1.0 + double(xa[i]) * stv, ne = 1.0 + double(xe[i]) * seal;
+          stv = i > jj ? nt : stv;
+          seal = i > jj ? ne : seal;
         }
         dt = float(ptv * stv);
         de = float(peal * seal);
@@ -668,8 +674,8 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           double pt = 1.0, pe = 1.0;
 #pragma unroll
           for (int q = 0; q < K; ++q) {
-            pt *= double(sh_a[o0 + q][0]);
-            pe *= double(sh_a[o0 + q][1]);
+            pt *= double(xa[q]);
+            pe *= double(xe[q]);
             etv += pt;
             eeal += pe;
           }
