@@ -12,7 +12,8 @@
 //            member holds bit-identical row normalisers; EAL's a = q(x*)
 //            follows from the payload).
 //   phase B  (WTV) per-row partial sums of min(p, q) and Q< = sum_{q<p} q,
-//            published, merged in member order.
+//            published, merged in member order; the mask [q < p] of every
+//            element is kept as one bit per element for phase C.
 //   scan     prefix products / suffix sums over the K rows give E and the
 //            gradient coefficients (Eqs. eal_generic, loss_eal, loss_tv).
 //   phase C  gradient from the registers, 16-byte nontemporal stores; each
@@ -24,7 +25,12 @@
 // group's arithmetic: of the four merges of a window only the last one waits.
 // The first pairs of the next window are staged into LDS during phase A and
 // copied to the registers in phase C; each wave stages and reads back only
-// its own threads' slots, so no barrier separates consecutive windows.
+// its own threads' slots, so no barrier separates consecutive windows.  For
+// WTV the first row group's target is dead once its phase-B partials are
+// summed (phase C needs only the mask bits): its registers take their staged
+// next-window copies after the second phase-A merge, and the freed slots
+// stage most of the next window's remaining pairs, so phase C issues few HBM
+// loads besides its gradient stores.
 //
 // The grid is persistent and launched cooperatively, so every member of a
 // team is resident.  Partials travel as 64-bit words {value, tag}: a reader
@@ -90,6 +96,21 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
   constexpr int kLdsStage = kBlock >= 512 ? 144 * 1024 : 72 * 1024;  // one or two workgroups per CU
   constexpr int kPre = kPairs < kLdsStage / (2 * kBlock * 16) ? kPairs : kLdsStage / (2 * kBlock * 16);
   static_assert(kPre >= 1, "staging holds at least one pair");
+  // WTV splits the rows into two groups (K0 rows, then the rest).  Phase C
+  // reads no target (the mask bits replace it), so the target registers of
+  // the first group are refilled with the next window as soon as the second
+  // group's normalisers are merged, from their staged copies, and those
+  // staging slots then take the next window's unstaged target pairs and, as
+  // far as they go, its unstaged draft pairs: phase C, which carries the
+  // gradient stores, is left with few or no HBM loads.
+  constexpr int K0 = kWtv && K > 1 ? (K + 1) / 2 : K;
+  constexpr bool kEarly = kWtv && K0 < K;
+  constexpr int kFree = kEarly ? (K0 * NV < kPre ? K0 * NV : kPre) : 0;  // target slots refilled early
+  constexpr int kUnst = kPairs - kPre;                                 // unstaged pairs per tensor
+  // Restaging slot of unstaged pair i (i >= kPre) of the target / draft, or
+  // -1 when it still comes from HBM in phase C.
+  auto rslot_t = [](int i) { return (i - kPre) < kFree ? i - kPre : -1; };
+  auto rslot_d = [](int i) { return kUnst + (i - kPre) < kFree ? kUnst + (i - kPre) : -1; };
   __shared__ u32x4 sh_pre[kPre][2][kBlock];
   __shared__ float sh_w[kWaves][K][kC];  // per-wave partials
   __shared__ float sh_row[K][4];        // merged row constants
@@ -123,6 +144,20 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
   const int64_t slot_plane = int64_t(p.T) * K * p.W * 8;
 
   u32x4 rd[K][NV], rt[K][NV];
+  // WTV: phase B leaves [q < p] of every element in these bits for phase C,
+  // which then needs neither the target nor a compare.  Pair i = k NV + v
+  // holds bits in register i / kPairsPerReg, pushed in pair order.
+  constexpr int kPairsPerReg = 32 / E;
+  constexpr int kMaskRegs = kWtv ? (kPairs + kPairsPerReg - 1) / kPairsPerReg : 1;
+  uint32_t mbits[kMaskRegs];
+#pragma unroll
+  for (int r = 0; r < kMaskRegs; ++r) mbits[r] = 0u;
+  // bit position of element e of pair i once phase B is complete
+  auto mask_pos = [](int i, int e) {
+    const int r = i / kPairsPerReg;
+    const int n = (kPairs - r * kPairsPerReg < kPairsPerReg ? kPairs - r * kPairsPerReg : kPairsPerReg) * E;
+    return n - 1 - ((i % kPairsPerReg) * E + e);
+  };
 
   const uint32_t win_bytes = uint32_t(stride_w);
   auto pin_all = [&]() {
@@ -229,7 +264,10 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
           for (int v = 0; v < NV; ++v)
 #pragma unroll
-            for (int e = 0; e < E; ++e) sum += ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
+            for (int e = 0; e < E; ++e) {
+              const float x = ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
+              sum = (v == 0 && e == 0) ? x : sum + x;  // no add of the initial zero
+            }
         }
         m0[k] = m == kNegInf ? kNegInf : msc;
         s0[k] = sum;
@@ -247,7 +285,10 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
             for (int v = 0; v < NV; ++v)
 #pragma unroll
-              for (int e = 0; e < E; ++e) st += ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+              for (int e = 0; e < E; ++e) {
+                const float x = ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+                st = (v == 0 && e == 0) ? x : st + x;
+              }
           }
           m1[k] = mt == kNegInf ? kNegInf : mtsc;
           s1[k] = st;
@@ -409,8 +450,16 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
             const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
             const float t = __builtin_fmaf(xt[e], p.sct, -ct);
             const float mn = ex2(fminf(u, t));
-            sm += mn;
-            sq += (u < t) ? mn : 0.f;
+            // the compare below, as a lane mask (the compiler emits one v_cmp for both)
+            const uint64_t lt = __builtin_amdgcn_fcmpf(u, t, 4 /* ordered less-than */);
+            if (v == 0 && e == 0) {
+              sm = mn;
+              sq = (u < t) ? mn : 0.f;
+            } else {
+              sm += mn;
+              sq += (u < t) ? mn : 0.f;
+            }
+            push_bit(mbits[(k * NV + v) / kPairsPerReg], lt);
           }
         }
         am[k - k0] = sm;
@@ -469,7 +518,6 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     // slower members time to publish, so three of the four merges of a
     // window overlap arithmetic and only the last one waits.  EAL has one
     // merge per window and keeps a single group.
-    constexpr int K0 = kWtv && K > 1 ? (K + 1) / 2 : K;
     using I0 = std::integral_constant<int, 0>;
     using IK0 = std::integral_constant<int, K0>;
     using IK = std::integral_constant<int, K>;
@@ -492,6 +540,18 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       phase_b(I0{}, IK0{});
       merge_a(K0, K);
       lds_barrier();
+      // The first group's target is dead: take the next window's staged
+      // copies into its registers, then restage the freed slots.
+      wait_vmem_all();  // this window's staging (issued in phase A) has landed
+#pragma unroll
+      for (int i = 0; i < kFree; ++i) rt[i / NV][i % NV] = sh_pre[i][1][tid];
+      wait_lds_all();  // the slots are read before the loads below rewrite them
+#pragma unroll
+      for (int s = 0; s < kFree; ++s) {
+        const int i = kPre + (s < kUnst ? s : s - kUnst);
+        if (i < kPairs)
+          bld16_lds(s < kUnst ? nt : nd, &sh_pre[s][1][wbase], coff[i % NV], (i / NV) * p.row_bytes);
+      }
       phase_b(IK0{}, IK{});
       merge_b(0, K);
       lds_barrier();
@@ -559,34 +619,31 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     const uint32_t grow = gw != nullptr ? p.grow_bytes : 0u;
     wait_vmem_all();  // staging has landed (issued a whole phase A and B earlier)
     pin_all();
+    float mscd = 0.f, cA = 0.f, cB = 0.f;
 #pragma unroll
     for (int j = 0; j < kPairs; ++j) {
       const int i = (j + kPre) % kPairs;
       const int k = i / NV, v = i % NV;
-      // q = 2^-l2sd 2^u: the row factor 2^-l2sd is folded into the coefficients
-      const float mscd = sh_row[k][0], rs = ex2(-sh_row[k][1]);
-      float ct = 0.f, cA, cB = 0.f;
-      if constexpr (kWtv) {
-        ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);  // as in phase B
-        cA = sh_coef[k][0] * rs;
-        cB = sh_coef[k][1] * rs;
-        // keep the products: the select below would otherwise absorb them and
-        // multiply every element by rs
-        asm volatile("" : "+v"(cA), "+v"(cB));
-      } else {
-        cA = -sh_coef[k][0] * rs;
+      if (j == 0 || v == 0) {  // a new row: its constants, once per row
+        // q = 2^-l2sd 2^u: the row factor 2^-l2sd is folded into the coefficients
+        const float rs = ex2(-sh_row[k][1]);
+        mscd = sh_row[k][0];
+        if constexpr (kWtv) {
+          cA = sh_coef[k][0] * rs;
+          cB = sh_coef[k][1] * rs;
+        } else {
+          cA = -sh_coef[k][0] * rs;
+        }
       }
       const rsrc_t gr = make_rsrc(gw + k * grow, grow);  // slots past the row end are dropped
       float xd[E], g[E];
       unpackv<TI, E>(rd[k][v], xd);
       if constexpr (kWtv) {
-        float xt[E];
-        unpackv<TI, E>(rt[k][v], xt);
+        // the mask [q < p] from phase B selects the coefficient
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
-          const float t = __builtin_fmaf(xt[e], p.sct, -ct);
-          g[e] = ex2(u) * ((u < t) ? cA : cB);
+          g[e] = ex2(u) * select_bit(mbits[i / kPairsPerReg], mask_pos(i, e), cA, cB);
         }
       } else {
         // -c q everywhere; the greedy token's entry is fixed up after the loop
@@ -597,10 +654,11 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       asm volatile("" ::: "memory");  // keep the refill below this slot's store
       if (i < kPre) {
         rd[k][v] = sh_pre[i][0][tid];
-        rt[k][v] = sh_pre[i][1][tid];
+        if (i >= kFree) rt[k][v] = sh_pre[i][1][tid];  // pairs below kFree were refilled after merge A
       } else {
-        rd[k][v] = bld16(nd, coff[v], k * p.row_bytes);
-        rt[k][v] = bld16(nt, coff[v], k * p.row_bytes);
+        const int sd = kEarly ? rslot_d(i) : -1, st = kEarly ? rslot_t(i) : -1;
+        rd[k][v] = sd >= 0 ? sh_pre[sd][1][tid] : bld16(nd, coff[v], k * p.row_bytes);
+        rt[k][v] = st >= 0 ? sh_pre[st][1][tid] : bld16(nt, coff[v], k * p.row_bytes);
       }
     }
     if constexpr (!kWtv) {

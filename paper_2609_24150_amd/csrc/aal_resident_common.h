@@ -95,6 +95,25 @@ __device__ __forceinline__ void unpackv(const u32x4& w, float (&x)[E]) {
   TI::unpack(make_uint4(w.x, w.y, w.z, w.w), x);
 }
 
+// Per-element mask bits kept in VGPRs between two phases.  push_bit appends
+// one bit per lane from a wave lane mask (the result of a compare) with a
+// single add-with-carry: bits = 2 bits + carry, so after n pushes the i-th
+// pushed bit (from 0) sits at position n - 1 - i.  The compiler rewrites
+// 2 bits + b as a shift and an OR of a selected constant (three or four
+// instructions), hence the inline assembly.
+__device__ __forceinline__ void push_bit(uint32_t& bits, uint64_t lanes) {
+  uint64_t carry_out;
+  asm("v_addc_co_u32_e64 %0, %1, %2, %2, %3" : "=v"(bits), "=s"(carry_out) : "v"(bits), "s"(lanes));
+}
+// a where bit `pos` of bits is set, else b: a sign-extended one-bit field
+// selects whole words through a bitfield insert.
+__device__ __forceinline__ float select_bit(uint32_t bits, int pos, float a, float b) {
+  const int32_t m = __builtin_amdgcn_sbfe(int32_t(bits), pos, 1);
+  float r;
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(a), "v"(b));
+  return r;
+}
+
 __device__ __forceinline__ uint64_t tagged(float v, uint32_t tag) {
   return (uint64_t(tag) << 32) | __builtin_bit_cast(uint32_t, v);
 }
