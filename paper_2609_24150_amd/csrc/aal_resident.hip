@@ -104,8 +104,8 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
   // far as they go, its unstaged draft pairs: phase C, which carries the
   // gradient stores, is left with few or no HBM loads.
   constexpr int K0 = kWtv && K > 1 ? (K + 1) / 2 : K;
-  constexpr bool kEarly = kWtv && K0 < K;
-  constexpr int kFree = kEarly ? (K0 * NV < kPre ? K0 * NV : kPre) : 0;  // target slots refilled early
+  constexpr bool kEarly = kWtv && K0 < K && K0 * NV <= kPre;  // the first group is wholly staged
+  constexpr int kFree = kEarly ? K0 * NV : 0;                    // target slots refilled early
   constexpr int kUnst = kPairs - kPre;                                 // unstaged pairs per tensor
   // Restaging slot of unstaged pair i (i >= kPre) of the target / draft, or
   // -1 when it still comes from HBM in phase C.
@@ -170,6 +170,53 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       }
   };
 
+  // WTV: the first group's target (max, sum-exp) partials of a window are
+  // evaluated one window ahead, while the previous window's last team merge
+  // is in flight (the registers hold the next window's target by then), so
+  // that wait is spent on arithmetic phase A would otherwise do.
+  // Used with a first group of 4 rows (K = 7, 8), where the partials fit
+  // beside the resident data: at K = 5 (3 rows, 13-member teams) it measured
+  // slower, and larger groups spill.
+#ifndef AAL_AHEAD_MIN_ROWS
+#define AAL_AHEAD_MIN_ROWS 4
+#endif
+#ifndef AAL_AHEAD_MAX_ROWS
+#define AAL_AHEAD_MAX_ROWS 4
+#endif
+  constexpr bool kAhead = kEarly && K0 >= AAL_AHEAD_MIN_ROWS && K0 <= AAL_AHEAD_MAX_ROWS;
+  constexpr int KE = kAhead ? K0 : 1;
+  float em[KE], es[KE];
+  auto target_partial = [&](int k, float& mo, float& so) {
+    float xs[NV][E];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
+    float mt = kNegInf;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+    const float mtsc = mt * p.sct;
+    float st = 0.f;
+    if (mt != kNegInf) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const float x = ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+          st = (v == 0 && e == 0) ? x : st + x;  // no add of the initial zero
+        }
+    }
+    mo = mt == kNegInf ? kNegInf : mtsc;
+    so = st;
+  };
+  // slots past the row end (last member only) hold copies of the row's last
+  // vector: mask them
+  auto mask_tail = [&](u32x4 (&r)[K][NV], int k) {
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+      if (col[v] >= p.ng) r[k][v] = neg_inf_vec(TI{});
+  };
+
   int64_t w = team;
   if (w < p.N) {
     // The first window arrives the way later windows do (staged pairs through
@@ -197,6 +244,13 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       rt[k][v] = sh_pre[i][1][tid];
     }
     __syncthreads();  // staging is read before the loop restages it
+    if constexpr (kAhead) {
+#pragma unroll
+      for (int k = 0; k < K0; ++k) {
+        if (last) mask_tail(rt, k);
+        target_partial(k, em[k], es[k]);
+      }
+    }
   }
   // read once: a global load inside the scan would sit on every window's
   // critical path
@@ -271,28 +325,16 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         }
         m0[k] = m == kNegInf ? kNegInf : msc;
         s0[k] = sum;
-#pragma unroll
-        for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
         if constexpr (kWtv) {
-          float mt = kNegInf;
-#pragma unroll
-          for (int v = 0; v < NV; ++v)
-#pragma unroll
-            for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
-          const float mtsc = mt * p.sct;
-          float st = 0.f;
-          if (mt != kNegInf) {
-#pragma unroll
-            for (int v = 0; v < NV; ++v)
-#pragma unroll
-              for (int e = 0; e < E; ++e) {
-                const float x = ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
-                st = (v == 0 && e == 0) ? x : st + x;
-              }
+          if (kAhead && k < K0) {  // evaluated during the previous window's last merge
+            m1[k] = em[k < KE ? k : 0];
+            s1[k] = es[k < KE ? k : 0];
+          } else {
+            target_partial(k, m1[k], s1[k]);
           }
-          m1[k] = mt == kNegInf ? kNegInf : mtsc;
-          s1[k] = st;
         } else {
+#pragma unroll
+          for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
           float best = kNegInf, bi, bz;
 #pragma unroll
           for (int v = 0; v < NV; ++v)
@@ -545,6 +587,10 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       wait_vmem_all();  // this window's staging (issued in phase A) has landed
 #pragma unroll
       for (int i = 0; i < kFree; ++i) rt[i / NV][i % NV] = sh_pre[i][1][tid];
+      if (last) {
+#pragma unroll
+        for (int k = 0; k < K0; ++k) mask_tail(rt, k);
+      }
       wait_lds_all();  // the slots are read before the loads below rewrite them
 #pragma unroll
       for (int s = 0; s < kFree; ++s) {
@@ -553,6 +599,13 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           bld16_lds(s < kUnst ? nt : nd, &sh_pre[s][1][wbase], coff[i % NV], (i / NV) * p.row_bytes);
       }
       phase_b(IK0{}, IK{});
+      // the next window's first-group target partials, while the other
+      // members' last partials are on their way (past the team's last window
+      // the registers hold zeros and the results go unused)
+      if constexpr (kAhead) {
+#pragma unroll
+        for (int k = 0; k < K0; ++k) target_partial(k, em[k], es[k]);
+      }
       merge_b(0, K);
       lds_barrier();
     }
