@@ -36,7 +36,13 @@
 // Variants with a phase B split the chunk's rows into two groups whose merges
 // overlap the other group's arithmetic, as in the EAL/WTV kernel, and no
 // barrier separates consecutive chunks (the staging buffer is per wave and
-// the label data is double-buffered by chunk parity).
+// the label data is double-buffered by chunk parity).  With a TV term and no
+// KL term, phase B keeps the mask [q < p] as bits and phase C reads no
+// target: the first group's target registers are refilled early and the
+// freed staging slots take most of the next chunk's unstaged pairs, and
+// (without the greedy token) that group's target partials of the next chunk
+// are evaluated while a wait is in flight: the last team merge for disjoint
+// windows, the neighbour exchange for sliding ones.
 //
 // Rows of a chunk past the end of its sequence (when K does not divide S)
 // load as zeros and store nothing.  Polls are bounded; a timeout sets the
@@ -113,6 +119,24 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   constexpr int kPre = kPairs < kLdsStage / (2 * kBlock * 16) ? kPairs : kLdsStage / (2 * kBlock * 16);
   constexpr float kLn2 = 0.693147180559945309417f;
   static_assert(kC * K <= kBlock && 2 * K <= kWave && K * K <= kBlock, "thread-per-item steps");
+  // Phase B, when present, splits the rows into two groups (K0 rows, then the
+  // rest).  With a TV term and no KL term phase C needs the target only for
+  // the mask [q < p], which phase B leaves in bits: the first group's target
+  // registers then take the next chunk's staged copies after the second
+  // phase-A merge, and the freed slots stage most of the next chunk's
+  // unstaged pairs, as in the EAL/WTV kernel.
+  constexpr int K0 = PQ && K > 1 ? (K + 1) / 2 : K;
+  constexpr bool MB = TV && !KL;
+  constexpr bool kEarly = MB && K0 < K && K0 * NV <= kPre;
+  constexpr int kFree = kEarly ? K0 * NV : 0;
+  constexpr int kUnst = kPairs - kPre;
+  // Without the greedy token (which phase A takes from the same target
+  // data), the first group's target partials of a chunk are evaluated during
+  // the previous chunk's last team merge, with a first group of 4 rows.
+  constexpr bool kAhead = kEarly && !AM && K0 == 4;
+  constexpr int KE = kAhead ? K0 : 1;
+  constexpr int kPairsPerReg = 32 / E;
+  constexpr int kMaskRegs = MB ? (kPairs + kPairsPerReg - 1) / kPairsPerReg : 1;
   __shared__ u32x4 sh_pre[kPre][2][kBlock];
   __shared__ float sh_w[kWaves][K][kC];
   __shared__ float sh_row[K][6];    // msc_d, l2s_d, msc_t, l2s_t, a_eal = q(x*), p(x*)
@@ -159,6 +183,48 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   };
 
   u32x4 rd[K][NV], rt[K][NV];
+  uint32_t mbits[kMaskRegs];
+#pragma unroll
+  for (int r = 0; r < kMaskRegs; ++r) mbits[r] = 0u;
+  // bit position of element e of pair i once phase B is complete (pair i's
+  // bits are pushed into register i / kPairsPerReg in pair order)
+  auto mask_pos = [](int i, int e) {
+    const int r = i / kPairsPerReg;
+    const int n = (kPairs - r * kPairsPerReg < kPairsPerReg ? kPairs - r * kPairsPerReg : kPairsPerReg) * E;
+    return n - 1 - ((i % kPairsPerReg) * E + e);
+  };
+  auto rslot_t = [](int i) { return (i - kPre) < kFree ? i - kPre : -1; };
+  auto rslot_d = [](int i) { return kUnst + (i - kPre) < kFree ? kUnst + (i - kPre) : -1; };
+  float em[KE], es[KE];
+  // the target's (max, sum-exp) partial of row k over this thread's columns
+  auto target_partial = [&](int k, float& mo, float& so) {
+    float xs[NV][E];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
+    float mt = kNegInf;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+    const float mtsc = mt * p.sct;
+    float st = 0.f;
+    if (mt != kNegInf) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const float x = ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+          st = (v == 0 && e == 0) ? x : st + x;
+        }
+    }
+    mo = mt == kNegInf ? kNegInf : mtsc;
+    so = st;
+  };
+  auto mask_tail = [&](u32x4 (&r)[K][NV], int k) {
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+      if (col[v] >= p.ng) r[k][v] = neg_inf_vec(TI{});
+  };
   auto pin_all = [&]() {
 #pragma unroll
     for (int k = 0; k < K; ++k)
@@ -198,6 +264,13 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       rt[k][v] = sh_pre[i][1][tid];
     }
     __syncthreads();
+    if constexpr (kAhead) {
+#pragma unroll
+      for (int k = 0; k < K0; ++k) {
+        if (last) mask_tail(rt, k);
+        target_partial(k, em[k], es[k]);
+      }
+    }
   }
   // read once: a global load inside the scan would sit on every chunk's
   // critical path
@@ -278,34 +351,46 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
 #pragma unroll
           for (int v = 0; v < NV; ++v)
 #pragma unroll
-            for (int e = 0; e < E; ++e) sum += ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
+            for (int e = 0; e < E; ++e) {
+              const float x = ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
+              sum = (v == 0 && e == 0) ? x : sum + x;  // no add of the initial zero
+            }
         }
         m0[k] = m == kNegInf ? kNegInf : msc;
         s0[k] = sum;
-#pragma unroll
-        for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
         m1[k] = kNegInf;
         s1[k] = 0.f;
-        float mt = kNegInf;  // the target's maximum (normaliser and greedy token)
-        if constexpr (PQ || AM) {
+        if constexpr (PQ && !AM) {
+          if (kAhead && k < K0) {  // evaluated during the previous chunk's last merge
+            m1[k] = em[k < KE ? k : 0];
+            s1[k] = es[k < KE ? k : 0];
+          } else {
+            target_partial(k, m1[k], s1[k]);
+          }
+        }
+        if constexpr (AM) {
+#pragma unroll
+          for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
+          float mt = kNegInf;  // the target's maximum (normaliser and greedy token)
 #pragma unroll
           for (int v = 0; v < NV; ++v)
 #pragma unroll
             for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
-        }
-        if constexpr (PQ) {
-          const float mtsc = mt * p.sct;
-          float st = 0.f;
-          if (mt != kNegInf) {
+          if constexpr (PQ) {
+            const float mtsc = mt * p.sct;
+            float st = 0.f;
+            if (mt != kNegInf) {
 #pragma unroll
-            for (int v = 0; v < NV; ++v)
+              for (int v = 0; v < NV; ++v)
 #pragma unroll
-              for (int e = 0; e < E; ++e) st += ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+                for (int e = 0; e < E; ++e) {
+                  const float x = ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+                  st = (v == 0 && e == 0) ? x : st + x;
+                }
+            }
+            m1[k] = mt == kNegInf ? kNegInf : mtsc;
+            s1[k] = st;
           }
-          m1[k] = mt == kNegInf ? kNegInf : mtsc;
-          s1[k] = st;
-        }
-        if constexpr (AM) {
           float best = mt, bi, bz;
           first_max<TI, NV, E, kBlock>(xs, rd[k], mt, col[0] * E, bi, bz);
           wave_argmax(best, bi, bz);
@@ -499,6 +584,10 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
               const float mn = ex2(fminf(u, t));
               sm += mn;
               sq += (u < t) ? mn : 0.f;
+              if constexpr (MB) {
+                // the compare above as a lane mask (one v_cmp serves both)
+                push_bit(mbits[(k * NV + v) / kPairsPerReg], __builtin_amdgcn_fcmpf(u, t, 4 /* ordered less-than */));
+              }
             }
             if constexpr (KL) {
               const float ep = ex2(t);  // p 2^l2s_d; p = 0 contributes nothing
@@ -581,7 +670,6 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
     // pipelined: each group's partials are published as soon as they are
     // complete and a merge is polled only after the other group's
     // arithmetic, so three of the four merges of a chunk overlap arithmetic.
-    constexpr int K0 = PQ && K > 1 ? (K + 1) / 2 : K;
     using I0 = std::integral_constant<int, 0>;
     using IK0 = std::integral_constant<int, K0>;
     using IK = std::integral_constant<int, K>;
@@ -607,7 +695,36 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       phase_b(I0{}, IK0{});
       merge_a(K0, K);
       lds_barrier();
+      if constexpr (kEarly) {
+        // the first group's target is dead: the next chunk's staged copies go
+        // to its registers, then the freed slots are restaged
+        wait_vmem_all();  // this chunk's staging (issued in phase A) has landed
+#pragma unroll
+        for (int i = 0; i < kFree; ++i) rt[i / NV][i % NV] = sh_pre[i][1][tid];
+        if (last) {
+#pragma unroll
+          for (int k = 0; k < K0; ++k) mask_tail(rt, k);
+        }
+        wait_lds_all();  // the slots are read before the loads below rewrite them
+#pragma unroll
+        for (int s = 0; s < kFree; ++s) {
+          const int i = kPre + (s < kUnst ? s : s - kUnst);
+          if (i < kPairs)
+            bld16_lds(s < kUnst ? nt : nd, &sh_pre[s][1][wbase], coff[i % NV], (i / NV) * p.row_bytes);
+        }
+      }
       phase_b(IK0{}, IK{});
+      if constexpr (kAhead) {
+        // the next chunk's first-group target partials while the other
+        // members' last partials are on their way (past the team's last chunk
+        // the registers hold zeros and the results go unused); with windows
+        // sliding over sequences they wait for the neighbour exchange below
+        // instead, whose wait sits on the cycle that paces the teams
+        if (p.CS == 1) {
+#pragma unroll
+          for (int k = 0; k < K0; ++k) target_partial(k, em[k], es[k]);
+        }
+      }
       merge_b(0, K);
     }
     lds_barrier();
@@ -623,6 +740,10 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         uint64_t* const ar = p.arow + (row0 + tid) * 2;
         publish(ar, sh_b[tid][0], 1u);
         publish(ar + 1, sh_row[tid][4], 1u);
+      }
+      if constexpr (kAhead) {
+#pragma unroll
+        for (int k = 0; k < K0; ++k) target_partial(k, em[k], es[k]);
       }
       if (wv == 0 && lane < 2 * K) {
         const int o = lane < K ? lane - K : lane;  // offset from row0: -K..-1, K..2K-1
@@ -739,19 +860,30 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
     for (int k = 0; k < K; ++k) klp[k] = 0.f;
     wait_vmem_all();  // staging has landed
     pin_all();
+    float mscd = 0.f, ct = 0.f, cA = 0.f, cB = 0.f, cP = 0.f;
 #pragma unroll
     for (int jp = 0; jp < kPairs; ++jp) {
       const int i = (jp + kPre) % kPairs;
       const int k = i / NV, v = i % NV;
-      const float mscd = sh_row[k][0];
-      const float ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
-      float cA = sh_coef[k][0], cB = sh_coef[k][1];
-      asm volatile("" : "+v"(cA), "+v"(cB));
-      const float cP = sh_coef[k][2];
+      if (jp == 0 || v == 0) {  // a new row: its constants, once per row
+        mscd = sh_row[k][0];
+        ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
+        cA = sh_coef[k][0];
+        cB = sh_coef[k][1];
+        if constexpr (!MB) asm volatile("" : "+v"(cA), "+v"(cB));
+        cP = sh_coef[k][2];
+      }
       const rsrc_t gr = make_rsrc(gw + k * p.grow_bytes, gw != nullptr && k < nvalid ? p.grow_bytes : 0u);
       float xd[E], g[E];
       unpackv<TI, E>(rd[k][v], xd);
-      if constexpr (PQ) {
+      if constexpr (MB) {
+        // the mask [q < p] from phase B selects the coefficient
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const float u = __builtin_fmaf(xd[e], p.scd, -mscd);
+          g[e] = ex2(u) * select_bit(mbits[i / kPairsPerReg], mask_pos(i, e), cA, cB);
+        }
+      } else if constexpr (PQ) {
         float xt[E];
         unpackv<TI, E>(rt[k][v], xt);
 #pragma unroll
@@ -777,10 +909,11 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       asm volatile("" ::: "memory");
       if (i < kPre) {
         rd[k][v] = sh_pre[i][0][tid];
-        rt[k][v] = sh_pre[i][1][tid];
+        if (i >= kFree) rt[k][v] = sh_pre[i][1][tid];  // pairs below kFree were refilled after merge A
       } else {
-        rd[k][v] = bld16(nd, coff[v], k * p.row_bytes);
-        rt[k][v] = bld16(nt, coff[v], k * p.row_bytes);
+        const int sd = kEarly ? rslot_d(i) : -1, st = kEarly ? rslot_t(i) : -1;
+        rd[k][v] = sd >= 0 ? sh_pre[sd][1][tid] : bld16(nd, coff[v], k * p.row_bytes);
+        rt[k][v] = st >= 0 ? sh_pre[st][1][tid] : bld16(nt, coff[v], k * p.row_bytes);
       }
       if constexpr (KLC) {
         // the last pair of row k in this order: (jp + kPre) % kPairs runs
