@@ -111,7 +111,10 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
   // -1 when it still comes from HBM in phase C.
   auto rslot_t = [](int i) { return (i - kPre) < kFree ? i - kPre : -1; };
   auto rslot_d = [](int i) { return kUnst + (i - kPre) < kFree ? kUnst + (i - kPre) : -1; };
-  __shared__ u32x4 sh_pre[kPre][2][kBlock];
+  // staging slots of the draft and of the target, as separate arrays so that
+  // reads of draft slots are visibly independent of loads into target slots
+  __shared__ u32x4 sh_pre_d[kPre][kBlock];
+  __shared__ u32x4 sh_pre_t[kPre][kBlock];
   __shared__ float sh_w[kWaves][K][kC];  // per-wave partials
   __shared__ float sh_row[K][4];        // merged row constants
   __shared__ float sh_coef[K][2];       // gradient coefficients
@@ -227,8 +230,8 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
       const int k = i / NV, v = i % NV;
-      bld16_lds(bd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
-      bld16_lds(bt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+      bld16_lds(bd, &sh_pre_d[i][wbase], coff[v], k * p.row_bytes);
+      bld16_lds(bt, &sh_pre_t[i][wbase], coff[v], k * p.row_bytes);
     }
 #pragma unroll
     for (int i = kPre; i < kPairs; ++i) {
@@ -240,8 +243,8 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
       const int k = i / NV, v = i % NV;
-      rd[k][v] = sh_pre[i][0][tid];
-      rt[k][v] = sh_pre[i][1][tid];
+      rd[k][v] = sh_pre_d[i][tid];
+      rt[k][v] = sh_pre_t[i][tid];
     }
     __syncthreads();  // staging is read before the loop restages it
     if constexpr (kAhead) {
@@ -277,8 +280,8 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       for (int v = 0; v < NV; ++v) {
         const int i = k * NV + v;
         if (i < kPre) {
-          bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
-          bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+          bld16_lds(nd, &sh_pre_d[i][wbase], coff[v], k * p.row_bytes);
+          bld16_lds(nt, &sh_pre_t[i][wbase], coff[v], k * p.row_bytes);
         }
       }
     };
@@ -404,8 +407,15 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         }
       }
       lds_barrier();
-      if (tid < kC * KG) {  // merge the waves (fixed order), publish one component each
-        const int k = k0 + tid / kC, c = tid % kC;
+      // merge the waves (fixed order), publish one component each: the last
+      // threads of the workgroup when the next merge (of the first group's
+      // rows, polled by waves 0, 1, ...) leaves the last wave idle, so that
+      // the polling waves start at once; otherwise the first threads
+      constexpr int kPolled = K0 < K ? K0 : K;
+      constexpr int kPub0 = kPolled < kWaves ? kBlock - kC * KG : 0;
+      if (tid >= kPub0 && tid < kPub0 + kC * KG) {
+        const int pt = tid - kPub0;
+        const int k = k0 + pt / kC, c = pt % kC;
         float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
         float a4 = kWtv ? 0.f : sh_w[0][k][kC - 1];
 #pragma unroll
@@ -528,8 +538,13 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         }
       }
       lds_barrier();
-      if (tid < 2 * KG) {
-        const int k = k0 + (tid >> 1), c = tid & 1;
+      // the last threads when the next merge (of rows [k1 < K ? k1 : 0, K))
+      // leaves the last wave idle, as in phase A
+      constexpr int kPolled = k1 < K ? K - k1 : K;
+      constexpr int kPub0 = kPolled < kWaves ? kBlock - 2 * KG : 0;
+      if (tid >= kPub0 && tid < kPub0 + 2 * KG) {
+        const int pt = tid - kPub0;
+        const int k = k0 + (pt >> 1), c = pt & 1;
         float r = sh_w[0][k][c];
 #pragma unroll
         for (int i = 1; i < kWaves; ++i) r += sh_w[i][k][c];
@@ -586,7 +601,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       // copies into its registers, then restage the freed slots.
       wait_vmem_all();  // this window's staging (issued in phase A) has landed
 #pragma unroll
-      for (int i = 0; i < kFree; ++i) rt[i / NV][i % NV] = sh_pre[i][1][tid];
+      for (int i = 0; i < kFree; ++i) rt[i / NV][i % NV] = sh_pre_t[i][tid];
       if (last) {
 #pragma unroll
         for (int k = 0; k < K0; ++k) mask_tail(rt, k);
@@ -596,7 +611,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       for (int s = 0; s < kFree; ++s) {
         const int i = kPre + (s < kUnst ? s : s - kUnst);
         if (i < kPairs)
-          bld16_lds(s < kUnst ? nt : nd, &sh_pre[s][1][wbase], coff[i % NV], (i / NV) * p.row_bytes);
+          bld16_lds(s < kUnst ? nt : nd, &sh_pre_t[s][wbase], coff[i % NV], (i / NV) * p.row_bytes);
       }
       phase_b(IK0{}, IK{});
       // the next window's first-group target partials, while the other
@@ -670,14 +685,58 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     // without a gradient output the stores go to an empty resource (dropped)
     uint8_t* const gw = p.grad ? p.grad + w * int64_t(K) * p.grow_bytes : nullptr;
     const uint32_t grow = gw != nullptr ? p.grow_bytes : 0u;
-    wait_vmem_all();  // staging has landed (issued a whole phase A and B earlier)
+    // Order of the pairs.  Without restaging: the unstaged pairs first, from
+    // HBM (the longest time to land), then the staged ones.  With restaging:
+    //   C0  the pairs whose draft still comes from HBM (issued first: the
+    //       next window's phase A waits for them);
+    //   C1  the pairs staged in phase A, whose loads were issued before the
+    //       restaging loads: a wave that did not poll the last merge may still
+    //       have those in flight (the polls drained the others'), so waiting
+    //       down to that many suffices;
+    //   then one wait bounded by the stores and loads issued since the
+    //   restaging, the target refills that read restaged slots (or staged
+    //   slots beyond the first group), and
+    //   C2  the pairs whose draft was restaged.
+    constexpr int kStoresPerPair = (GS == 4 && E == 8) ? 2 : 1;
+    constexpr int kRestOps = kEarly ? (kFree < 2 * kUnst ? kFree : 2 * kUnst) : 0;
+    constexpr int kRD = kEarly ? (kFree - kUnst < 0 ? 0 : (kFree - kUnst < kUnst ? kFree - kUnst : kUnst)) : 0;
+    constexpr int kC0 = kEarly ? kUnst - kRD : 0;  // pairs kPre + kRD .. kPairs - 1
+    auto c_order = [](int j) {
+      if constexpr (!kEarly) {
+        return (j + kPre) % kPairs;
+      } else {
+        return j < kC0 ? kPre + kRD + j : j < kC0 + kPre ? j - kC0 : kPre + (j - kC0 - kPre);
+      }
+    };
+    // loads of a C0 pair: the draft, and the target when its slot was not restaged
+    auto c0_ops = []() {
+      int n = 0;
+      for (int i = kPre + kRD; i < kPairs; ++i) n += kStoresPerPair + 1 + ((i - kPre) >= kFree ? 1 : 0);
+      return n;
+    };
+    constexpr int kOpsAfterRestage = kEarly ? c0_ops() + kPre * kStoresPerPair : 0;
+    static_assert(kOpsAfterRestage < 64, "vmcnt range");
+    auto restaged_reads = [&]() {
+      wait_vmem_le<kOpsAfterRestage>();  // the restaging loads have landed
+#pragma unroll
+      for (int i2 = kFree; i2 < kPre; ++i2) rt[i2 / NV][i2 % NV] = sh_pre_t[i2][tid];
+#pragma unroll
+      for (int i2 = kPre + kRD; i2 < kPairs; ++i2)
+        if (i2 - kPre < kFree) rt[i2 / NV][i2 % NV] = sh_pre_t[i2 - kPre][tid];
+    };
+    if constexpr (kEarly) {
+      wait_vmem_le<kRestOps>();
+    } else {
+      wait_vmem_all();  // staging has landed (issued a whole phase A and B earlier)
+    }
     pin_all();
     float mscd = 0.f, cA = 0.f, cB = 0.f;
 #pragma unroll
     for (int j = 0; j < kPairs; ++j) {
-      const int i = (j + kPre) % kPairs;
+      const int i = c_order(j);
+      if (kEarly && j == kC0 + kPre) restaged_reads();
       const int k = i / NV, v = i % NV;
-      if (j == 0 || v == 0) {  // a new row: its constants, once per row
+      if (j == 0 || v == 0 || j == kC0) {  // a new row: its constants, once per row
         // q = 2^-l2sd 2^u: the row factor 2^-l2sd is folded into the coefficients
         const float rs = ex2(-sh_row[k][1]);
         mscd = sh_row[k][0];
@@ -706,14 +765,21 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       store_g<TG, E>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
       asm volatile("" ::: "memory");  // keep the refill below this slot's store
       if (i < kPre) {
-        rd[k][v] = sh_pre[i][0][tid];
-        if (i >= kFree) rt[k][v] = sh_pre[i][1][tid];  // pairs below kFree were refilled after merge A
+        rd[k][v] = sh_pre_d[i][tid];
+        // target pairs below kFree were refilled after merge A; with restaging
+        // the others are read after the wait above
+        if (!kEarly) rt[k][v] = sh_pre_t[i][tid];
       } else {
         const int sd = kEarly ? rslot_d(i) : -1, st = kEarly ? rslot_t(i) : -1;
-        rd[k][v] = sd >= 0 ? sh_pre[sd][1][tid] : bld16(nd, coff[v], k * p.row_bytes);
-        rt[k][v] = st >= 0 ? sh_pre[st][1][tid] : bld16(nt, coff[v], k * p.row_bytes);
+        rd[k][v] = sd >= 0 ? sh_pre_t[sd][tid] : bld16(nd, coff[v], k * p.row_bytes);
+        if (st < 0) {
+          rt[k][v] = bld16(nt, coff[v], k * p.row_bytes);
+        } else if (j >= kC0 + kPre) {  // C2 (a C0 pair's restaged target is read after the wait)
+          rt[k][v] = sh_pre_t[st][tid];
+        }
       }
     }
+    if constexpr (kEarly && kRD == 0) restaged_reads();  // no C2: the wait closes the phase
     if constexpr (!kWtv) {
       // EAL: the greedy token's entry is c (1 - q(x*)) = c (1 - a), written by
       // the thread whose vector store covered it (same thread, so it lands last)

@@ -44,6 +44,15 @@ __device__ __forceinline__ void bld16_lds(rsrc_t r, void* dst, uint32_t voff, ui
 // s_waitcnt vmcnt(0) as an instruction the compiler's wait-count tracking sees
 // (gfx9 encoding: vmcnt 0, expcnt 7, lgkmcnt 15).
 __device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// s_waitcnt vmcnt(N): at most N of the wave's vector-memory instructions are
+// outstanding.  They complete in issue order, so every instruction issued
+// before the last N has completed (loads into LDS included, which the
+// compiler's own wait counts do not track).
+template <int N>
+__device__ __forceinline__ void wait_vmem_le() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | 0x0F70 | ((N >> 4) << 14));
+}
 // s_waitcnt lgkmcnt(0) alone (vmcnt 63, expcnt 7): the wave's LDS reads have
 // completed.
 __device__ __forceinline__ void wait_lds_all() { __builtin_amdgcn_s_waitcnt(0xC07F); }
