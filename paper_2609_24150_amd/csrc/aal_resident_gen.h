@@ -473,8 +473,16 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           publish(prev_slots + (int64_t(tid) * p.W + member) * kGenSlotWords + kKlWord, r, 2u * iter);
         }
       }
-      if (tid < kC * KG) {
-        const int k = k0 + tid / kC, cc = tid % kC;
+      // merge the waves, publish one component each.  With pipelined merges
+      // (a phase B) the last threads of the workgroup publish when the next
+      // merge (polled by waves 0, 1, ...) leaves the last wave idle, so that
+      // the polling waves start at once; with a single merge right after
+      // phase A the publication itself is what every member waits for, and
+      // the first wave (which the SIMDs favour) publishes it sooner.
+      constexpr int kPolled = K0 < K ? K0 : K;
+      constexpr int kPub0 = (HB && kPolled < kWaves) ? kBlock - kC * KG : 0;
+      if (tid >= kPub0 && tid < kPub0 + kC * KG) {
+        const int k = k0 + (tid - kPub0) / kC, cc = (tid - kPub0) % kC;
         float a0 = sh_w[0][k][0], a1 = sh_w[0][k][1], a2 = sh_w[0][k][2], a3 = sh_w[0][k][3];
         float a4 = 0.f, a5 = 0.f, a6 = 0.f;
         if constexpr (AM) {
@@ -636,8 +644,10 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         }
       }
       lds_barrier();
-      if (tid < 3 * KG) {
-        const int k = k0 + tid / 3, cc = tid % 3;
+      constexpr int kPolledB = k1 < K ? K - k1 : K;  // rows of the next merge
+      constexpr int kPubB = kPolledB < kWaves ? kBlock - 3 * KG : 0;
+      if (tid >= kPubB && tid < kPubB + 3 * KG) {
+        const int k = k0 + (tid - kPubB) / 3, cc = (tid - kPubB) % 3;
         float r = sh_w[0][k][cc];
 #pragma unroll
         for (int i = 1; i < kWaves; ++i) r += sh_w[i][k][cc];
