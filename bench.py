@@ -462,7 +462,9 @@ def main():
         "practical_ceilings": ceilings(dev),
     }
     if args.copy_calibration:
-        src = torch.empty(1 << 32, dtype=torch.uint8, device=dev)
+        # the shape of the ceiling legs' copy (2^31 bf16 elements): a byte copy of exactly 2^32
+        # elements has been seen to read and write several times its size in the counters
+        src = torch.empty(1 << 31, dtype=torch.bfloat16, device=dev)
         dst = torch.empty_like(src)
         src.fill_(1)
         torch.cuda.synchronize()
