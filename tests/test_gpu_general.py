@@ -110,6 +110,17 @@ def test_sequence_edges(A, S, K, V, flags):
     _check(A, zd, zt, K, (0.7, 0.4, 1.3, 0.9), SEQ, Td=0.7, Tt=0.7, flags=flags)
 
 
+@pytest.mark.parametrize("S,K", [(16, 8), (17, 8), (23, 7), (40, 16), (9, 6), (13, 6)])
+@pytest.mark.parametrize("weights", [(1, 0, 0, 0), (0, 0, 0, 1), (1, 0.5, 0, 0)])
+def test_sequence_edges_tv_without_kl(A, S, K, weights, flags):
+    """A TV term and no KL term: the resident schedule keeps [q < p] as bits
+    from phase B, refills the target early and (K = 7, 8, no greedy token)
+    evaluates the next chunk's first-group target partials ahead; sequences
+    whose length K does not divide, on a vocabulary of several members."""
+    zd, zt = _inputs(3, S, 20480, torch.bfloat16, seed=5 + S + K)
+    _check(A, zd, zt, K, weights, SEQ, Td=0.9, Tt=0.9, flags=flags)
+
+
 @pytest.mark.parametrize("V", [1, 3, 8, 130, 2047, 2051, 2056])
 def test_ragged_vocab(A, V, flags):
     zd, zt = _inputs(2, 6, V, torch.bfloat16, seed=10 + V, peaks=V > 8)

@@ -68,7 +68,11 @@ def _check_wtv(A, zd, zt, Td, Tt, gdtype, flags, scale=None):
 # (V, K, N) spanning: V below one vector, ragged vectors, exact vector multiples,
 # several 256-thread tiles with ragged tails, and the workloads' vocabularies.
 SHAPES = [(1, 1, 3), (2, 2, 3), (3, 7, 2), (7, 3, 3), (8, 4, 2), (9, 2, 3), (1023, 4, 3),
-          (1024, 4, 5), (1025, 7, 3), (4099, 2, 2), (32000, 16, 2), (128256, 7, 1), (151936, 5, 1)]
+          (1024, 4, 5), (1025, 7, 3), (4099, 2, 2), (32000, 16, 2), (128256, 7, 1), (151936, 5, 1),
+          # K = 6 and 8 on teams of several members: the fused WTV schedule splits their
+          # unstaged pairs differently (at K = 6 every unstaged draft pair is restaged; at
+          # K = 8 the first row group's target partials are evaluated one window ahead)
+          (20000, 6, 3), (32000, 8, 2)]
 
 
 @pytest.mark.parametrize("path", ["auto", "stream"])
@@ -91,7 +95,8 @@ def test_wtv_parity_shapes(A, dev, V, K, N, dtype, gdtype, path):
 # windows per team, so the fused schedule runs several windows per team (the
 # alternating slot planes, the row-group merges and the windows that follow
 # each other without a barrier), checked element by element.
-MANY = [(BF16, BF16, 1024, 7, 700), (BF16, F32, 4096, 5, 600), (F32, F32, 2048, 16, 800)]
+MANY = [(BF16, BF16, 1024, 7, 700), (BF16, F32, 4096, 5, 600), (F32, F32, 2048, 16, 800),
+        (BF16, BF16, 2048, 8, 500), (F32, BF16, 1024, 6, 600), (BF16, BF16, 8192, 4, 400)]
 
 
 @pytest.mark.parametrize("dtype,gdtype,V,K,N", MANY)
