@@ -455,7 +455,7 @@ def main():
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
                      "algorithmic_bytes": alg_bytes,
                      "kernel": "k_resident (timed: the whole aal_wtv_fwd_bwd call, i.e. k_resident plus "
-                               "three microsecond-scale set-up/reduction kernels)",
+                               "two microsecond-scale kernels: slot clear, loss reduction)",
                      "alu": alu_roofline(prof, ms, alg_bytes)},
         "cpu_baseline": cpu,
         "validation": valid,

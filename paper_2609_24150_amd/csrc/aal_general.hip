@@ -307,7 +307,8 @@ __global__ __launch_bounds__(kBlock) void k_gen_loss_parts(const GenStats* __res
 }
 
 __global__ void k_gen_loss(const double* __restrict__ parts, int64_t R, int64_t W, int K, float w_wtv, float w_eal,
-                           float w_kl, float w_tv, float* __restrict__ loss, float* __restrict__ terms) {
+                           float w_kl, float w_tv, float* __restrict__ loss, float* __restrict__ terms,
+                           const unsigned* __restrict__ err) {
   if (threadIdx.x == 0) {
     double etv = 0.0, eeal = 0.0, kl = 0.0, tvs = 0.0;
     for (int b = 0; b < kGenLossParts; ++b) {
@@ -321,7 +322,10 @@ __global__ void k_gen_loss(const double* __restrict__ parts, int64_t R, int64_t 
     const double t1 = W > 0 && w_eal != 0.f ? -eeal / double(W) : 0.0;
     const double t2 = w_kl != 0.f ? kl / double(R) : 0.0;
     const double t3 = W > 0 && w_tv != 0.f ? tvs / (double(W) * K) : 0.0;
-    loss[0] = float(double(w_wtv) * t0 + double(w_eal) * t1 + double(w_kl) * t2 + double(w_tv) * t3);
+    // a set error word (a resident kernel's poll timed out): NaN
+    loss[0] = (err != nullptr && *err != 0u) ? __builtin_nanf("")
+                                             : float(double(w_wtv) * t0 + double(w_eal) * t1 + double(w_kl) * t2 +
+                                                     double(w_tv) * t3);
     if (terms) {
       terms[0] = float(t0);
       terms[1] = float(t1);
@@ -440,10 +444,10 @@ hipError_t launch_typed(const GenArgs& a) {
 
 }  // namespace
 
-hipError_t launch_general_loss(const GenArgs& a) {
+hipError_t launch_general_loss(const GenArgs& a, const unsigned* err) {
   k_gen_loss_parts<<<kGenLossParts, kBlock, 0, a.stream>>>(a.stats, a.win_tv, a.win_eal, a.R, a.W, a.loss_parts);
   k_gen_loss<<<1, 64, 0, a.stream>>>(a.loss_parts, a.R, a.W, a.K, a.w_wtv, a.w_eal, a.w_kl, a.w_tv, a.loss,
-                                     a.terms);
+                                     a.terms, err);
   return hipGetLastError();
 }
 
@@ -459,8 +463,7 @@ hipError_t launch_general(const GenArgs& a) {
     bool used = false;
     if (hipError_t e = launch_general_resident(a, &used); e != hipSuccess) return e;
     if (used) {
-      if (hipError_t e = launch_general_loss(a); e != hipSuccess) return e;
-      return launch_general_poison(a);
+      return launch_general_loss(a, a.res_err);  // NaN loss if a poll timed out
     }
   }
   return a.in == DType::kBf16 ? launch_typed<Bf16>(a) : launch_typed<F32>(a);

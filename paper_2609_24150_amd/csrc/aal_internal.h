@@ -82,7 +82,8 @@ struct LossArgs {
 hipError_t launch_streaming(const LossArgs& a);
 
 // loss = -(1/N) sum_n window_e[n], one workgroup, fixed summation order.
-hipError_t launch_loss_reduce(const LossArgs& a);
+// err: the error word of a resident kernel (NaN loss when set), or null
+hipError_t launch_loss_reduce(const LossArgs& a, const unsigned* err = nullptr);
 
 // Register-resident single-kernel schedule.  Sets *used = false (and enqueues
 // nothing) when the shape is outside what it supports: V not a multiple of the 16-byte vector, K outside {1..8, 16}, a window too
@@ -164,10 +165,10 @@ hipError_t launch_general_resident(const GenArgs& a, bool* used);
 hipError_t launch_general_resident_bf16(const GenArgs& a, bool* used);  // bf16 logits
 hipError_t launch_general_resident_bf16_g32(const GenArgs& a, bool* used);  // bf16 logits, fp32 gradient
 hipError_t launch_general_resident_f32(const GenArgs& a, bool* used);   // fp32 logits
-hipError_t launch_general_poison(const GenArgs& a);
 // Loss reduction of the combined objective over the per-row and per-window
 // values in the workspace.
-hipError_t launch_general_loss(const GenArgs& a);
+// err: the error word of the resident kernel (NaN loss when set), or null
+hipError_t launch_general_loss(const GenArgs& a, const unsigned* err = nullptr);
 
 // Per-row quantities of the GRPO schedule.  32 bytes.
 struct GrpoRow {

@@ -807,11 +807,6 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
   wait_vmem_all();  // the last (empty) staging loads retire before the workgroup ends
 }
 
-// Marks the loss NaN if any poll timed out.
-__global__ void k_poison_loss(const unsigned* err, float* loss) {
-  if (threadIdx.x == 0 && *err != 0u) loss[0] = __builtin_nanf("");
-}
-
 // Zeroes the tag words (tag 0 never matches) and the error word.
 __global__ void k_clear(uint64_t* p, int64_t n) {
   for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
@@ -888,9 +883,7 @@ hipError_t launch_k(const LossArgs& a, bool* used) {
                                  a.stream);
   if (e != hipSuccess) return e;
   *used = true;
-  if ((e = launch_loss_reduce(a)) != hipSuccess) return e;
-  k_poison_loss<<<1, 64, 0, a.stream>>>(p.err, a.loss);
-  return hipGetLastError();
+  return launch_loss_reduce(a, p.err);  // NaN loss if a poll timed out
 }
 
 template <class TI, class TG, int MODE>

@@ -999,10 +999,6 @@ __global__ void k_gen_clear(uint64_t* p, int64_t n) {
     p[i] = 0;
 }
 
-__global__ void k_gen_poison(const unsigned* err, float* loss) {
-  if (threadIdx.x == 0 && *err != 0u) loss[0] = __builtin_nanf("");
-}
-
 template <class TI, class TG, int K, int VAR>
 hipError_t launch_kg(const GenArgs& a, bool* used) {
   constexpr int NV = (16 / K) > 0 ? (16 / K) : 1;

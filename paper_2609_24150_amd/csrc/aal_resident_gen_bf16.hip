@@ -11,9 +11,5 @@ hipError_t launch_general_resident_bf16(const GenArgs& a, bool* used) {
   return launch_tg<Bf16, GBf16>(a, used);
 }
 
-hipError_t launch_general_poison(const GenArgs& a) {
-  k_gen_poison<<<1, 64, 0, a.stream>>>(a.res_err, a.loss);
-  return hipGetLastError();
-}
 
 }  // namespace aal

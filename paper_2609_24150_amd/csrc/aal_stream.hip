@@ -184,8 +184,10 @@ __global__ __launch_bounds__(kBlock) void k_window_scan(RowStats* __restrict__ s
   window_e[n] = float(E);
 }
 
+// err (may be null): a resident kernel's error word; set, the loss is NaN (a
+// poll timed out and the per-window values are incomplete).
 __global__ __launch_bounds__(kBlock) void k_loss(const float* __restrict__ window_e, int64_t N,
-                                                 float* __restrict__ loss) {
+                                                 float* __restrict__ loss, const unsigned* __restrict__ err) {
   __shared__ double sh[kWaves];
   double acc = 0.0;
   for (int64_t i = threadIdx.x; i < N; i += kBlock) acc += double(window_e[i]);
@@ -195,7 +197,7 @@ __global__ __launch_bounds__(kBlock) void k_loss(const float* __restrict__ windo
   if (threadIdx.x == 0) {
     double t = sh[0];
     for (int i = 1; i < kWaves; ++i) t += sh[i];
-    loss[0] = float(-t / double(N));
+    loss[0] = (err != nullptr && *err != 0u) ? __builtin_nanf("") : float(-t / double(N));
   }
 }
 
@@ -261,7 +263,7 @@ hipError_t launch_typed(const LossArgs& a) {
   const unsigned wblocks = unsigned((a.N + kBlock - 1) / kBlock);
   k_window_scan<<<wblocks, kBlock, 0, a.stream>>>(a.ws.stats, a.N, a.K, M, a.inv_t_d, a.grad_scale, a.window_e,
                                                   a.accept, a.xstar);
-  k_loss<<<1, kBlock, 0, a.stream>>>(a.window_e, a.N, a.loss);
+  k_loss<<<1, kBlock, 0, a.stream>>>(a.window_e, a.N, a.loss, nullptr);
   if (a.grad) {
     if (a.gd == DType::kBf16) {
       if (vec)
@@ -284,8 +286,8 @@ hipError_t launch_typed(const LossArgs& a) {
 
 }  // namespace
 
-hipError_t launch_loss_reduce(const LossArgs& a) {
-  k_loss<<<1, kBlock, 0, a.stream>>>(a.window_e, a.N, a.loss);
+hipError_t launch_loss_reduce(const LossArgs& a, const unsigned* err) {
+  k_loss<<<1, kBlock, 0, a.stream>>>(a.window_e, a.N, a.loss, err);
   return hipGetLastError();
 }
 
