@@ -199,8 +199,9 @@ def check_outputs(fn, outs, name, e_max=None):
 
 def ceilings(dev, nbytes=1 << 32):
     """Practical HBM ceilings on this GPU from plain device kernels (torch's
-    copy, a two-input elementwise add, a full-tensor sum), each timed with HIP
-    events over 10 launches after 3 warm-up launches."""
+    copy, a two-input elementwise add, a full-tensor sum, and the library's
+    streaming probe for each traffic mix of the loss kernels), each timed with
+    HIP events over 10 launches after 3 warm-up launches."""
     import torch
     n = nbytes // 2
     a = torch.ones(n, dtype=torch.bfloat16, device=dev)
@@ -210,12 +211,26 @@ def ceilings(dev, nbytes=1 << 32):
     legs = {"read (sum of one bf16 tensor)": (lambda: torch.sum(a, dtype=torch.float32), nbytes),
             "copy (1 read, 1 write)": (lambda: c.copy_(a), 2 * nbytes),
             "2 reads, 1 write (a + b)": (lambda: torch.add(a, b, out=c), 3 * nbytes)}
+    # the library's streaming probe: the loss kernels' own access (16-byte nontemporal loads and
+    # stores) for each traffic mix the kernels have
+    import paper_2609_24150_amd as A
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    d = torch.ones(n, dtype=torch.bfloat16, device=dev)
+    legs.update({
+        "probe: 1 read": (lambda: A.aal_stream_probe([a], flag=flag), nbytes),
+        "probe: 3 reads (the GRPO row pass's mix)": (lambda: A.aal_stream_probe([a, b, d], flag=flag), 3 * nbytes),
+        "probe: 1 read, 1 write (the GRPO gradient pass's mix)": (lambda: A.aal_stream_probe([a], c), 2 * nbytes),
+        "probe: 2 reads, 1 write (the fused losses' mix)": (lambda: A.aal_stream_probe([a, b], c), 3 * nbytes),
+    })
     res = {}
     for name, (fn, by) in legs.items():
         ms = _time_calls(fn, 10, 3, st)
         res[name] = {"GBps": by / (ms * 1e-3) / 1e9, "frac_of_peak": by / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
                      "bytes": by}
-    del a, b, c
+    torch.cuda.synchronize()
+    if flag.item() != 0:
+        _fail("the streaming probe saw a word it should not have")
+    del a, b, c, d
     _free_gpu(torch)
     return res
 

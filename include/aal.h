@@ -511,6 +511,21 @@ aal_status_t aal_vp_grad(const void* z_draft, const void* z_target, aal_dtype_t 
                          float temp_draft, float temp_target, const aal_vp_row_t* row,
                          void* grad_draft, aal_dtype_t grad_dtype, hipStream_t stream);
 
+/*
+ * Measurement aid, not part of the method: streams 1 to 3 device buffers of
+ * `bytes` bytes each (src0, then src1 and src2 when non-NULL) with 16-byte
+ * nontemporal loads -- the access the loss kernels use -- and, when dst is not
+ * NULL, writes their element-wise 32-bit wrapping sum to dst (`bytes` bytes),
+ * so that a timed call gives this device's practical HBM rate for a mix of
+ * reads and zero or one write.  Without dst, *flag ([1] uint32) is set to 1
+ * only where a summed 64-bit word is all ones, a data-dependent store that
+ * keeps every load live; fill the sources so that it does not happen.
+ * bytes : a positive multiple of 16.  Pointers 16-byte aligned (flag 4-byte);
+ * dst may alias none of the sources.  Four 256-thread workgroups per CU.
+ */
+aal_status_t aal_stream_probe(const void* src0, const void* src1, const void* src2, void* dst, size_t bytes,
+                              uint32_t* flag, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

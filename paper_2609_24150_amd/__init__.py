@@ -18,6 +18,7 @@ from .api import (  # noqa: F401
     aal_loss_fwd_bwd,
     aal_loss_workspace_bytes,
     aal_sim_accept_grpo,
+    aal_stream_probe,
     aal_vp_accept_partials,
     aal_vp_grad,
     aal_vp_merge_rows,

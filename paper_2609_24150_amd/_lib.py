@@ -102,6 +102,7 @@ _SIGNATURES = {
         _vp, _vp, C.c_int32, C.c_int64, C.c_int32, C.c_int, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp]),
     "aal_vp_sequence_scan": (C.c_int, [
         _vp, _vp, C.c_int32, C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_float, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "aal_stream_probe": (C.c_int, [_vp, _vp, _vp, _vp, C.c_size_t, _vp, _vp]),
     "aal_vp_grad": (C.c_int, [
         _vp, _vp, C.c_int, C.c_int64, C.c_int32, C.c_int32, C.c_int, C.c_float, C.c_float, _vp, _vp, C.c_int,
         _vp]),

@@ -426,3 +426,23 @@ def aal_vp_grad(z_draft: torch.Tensor, z_target: torch.Tensor | None, row: torch
                                 _dtype_code(g.dtype), _stream(dev, stream))
     _lib.check(st, "aal_vp_grad")
     return g
+
+
+def aal_stream_probe(srcs, dst: torch.Tensor | None = None, flag: torch.Tensor | None = None, stream=None):
+    """Measurement aid: stream 1-3 equally sized device tensors (16-byte
+    nontemporal loads) and, with dst, write their 32-bit wrapping sum there;
+    without dst, flag ([1] int32/uint32) is set only where a sum is all ones.
+    Enqueues and returns; time it with events on `stream`."""
+    srcs = list(srcs)
+    if not 1 <= len(srcs) <= 3:
+        raise ValueError("one to three sources")
+    nbytes = srcs[0].numel() * srcs[0].element_size()
+    for t in srcs + ([dst] if dst is not None else []):
+        if not t.is_cuda or not t.is_contiguous() or t.numel() * t.element_size() != nbytes:
+            raise ValueError("sources and dst must be contiguous device tensors of one size")
+    if dst is None and flag is None:
+        raise ValueError("flag is required without dst")
+    ptrs = [_ptr(t) for t in srcs] + [None] * (3 - len(srcs))
+    st = _lib.lib().aal_stream_probe(ptrs[0], ptrs[1], ptrs[2], _ptr(dst), nbytes, _ptr(flag),
+                                     _stream(srcs[0].device, stream))
+    _lib.check(st, "aal_stream_probe")

@@ -771,4 +771,23 @@ aal_status_t aal_vp_grad(const void* z_draft, const void* z_target, aal_dtype_t 
   return AAL_OK;
 }
 
+aal_status_t aal_stream_probe(const void* src0, const void* src1, const void* src2, void* dst, size_t bytes,
+                              uint32_t* flag, hipStream_t stream) {
+  clear_error();
+  if (!src0) return fail(AAL_ERR_ARG, "src0 must be non-NULL");
+  if (src2 && !src1) return fail(AAL_ERR_ARG, "src2 given without src1");
+  if (bytes == 0 || bytes % 16 != 0) return fail(AAL_ERR_ARG, "bytes must be a positive multiple of 16");
+  if (bytes / 16 >= (size_t(1) << 62)) return fail(AAL_ERR_ARG, "bytes too large");
+  if (!dst && !flag) return fail(AAL_ERR_ARG, "flag must be non-NULL when dst is NULL");
+  const void* src[3] = {src0, src1, src2};
+  for (const void* p : src)
+    if (p && !aligned(p, 16)) return fail(AAL_ERR_ALIGN, "sources must be 16-byte aligned");
+  if (dst && !aligned(dst, 16)) return fail(AAL_ERR_ALIGN, "dst must be 16-byte aligned");
+  if (flag && !aligned(flag, 4)) return fail(AAL_ERR_ALIGN, "flag must be 4-byte aligned");
+  const int n_src = src2 ? 3 : src1 ? 2 : 1;
+  const hipError_t e = aal::launch_stream_probe(src, n_src, dst, bytes, flag, stream);
+  if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return AAL_OK;
+}
+
 }  // extern "C"

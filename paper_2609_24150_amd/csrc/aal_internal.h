@@ -217,6 +217,11 @@ struct GrpoArgs {
 
 hipError_t launch_grpo(const GrpoArgs& a);
 
+// The streaming probe behind aal_stream_probe: n_src (1..3) sources of `bytes`
+// bytes each (a multiple of 16), summed into dst when dst is not null.
+hipError_t launch_stream_probe(const void* const src[3], int n_src, void* dst, size_t bytes, uint32_t* flag,
+                               hipStream_t stream);
+
 struct SimArgs {
   DType in;
   const void* zd;

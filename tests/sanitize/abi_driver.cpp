@@ -199,6 +199,16 @@ static void test_vp() {
   EXPECT(aal_vp_grad(D, D, AAL_BF16, 6, 64, 0, AAL_VP_WTV, 1.0f, 1.0f, row, D, AAL_BF16, nullptr), AAL_OK);
 }
 
+static void test_stream_probe() {
+  uint32_t flag = 0;
+  EXPECT(aal_stream_probe(D, D, nullptr, D, 4096, nullptr, nullptr), AAL_OK);
+  EXPECT(aal_stream_probe(D, nullptr, nullptr, nullptr, 4096, &flag, nullptr), AAL_OK);
+  EXPECT(aal_stream_probe(D, nullptr, nullptr, nullptr, 4096, nullptr, nullptr), AAL_ERR_ARG);  // no dst, no flag
+  EXPECT(aal_stream_probe(D, nullptr, D, D, 4096, nullptr, nullptr), AAL_ERR_ARG);              // src2 without src1
+  EXPECT(aal_stream_probe(D, D, D, D, 4095, nullptr, nullptr), AAL_ERR_ARG);                    // not 16-byte units
+  EXPECT(aal_stream_probe(nullptr, nullptr, nullptr, D, 4096, nullptr, nullptr), AAL_ERR_ARG);
+}
+
 static void test_noalloc() {
   // too large for the static scratch: rejected before the device is touched
   EXPECT(aal_wtv_fwd_bwd_noalloc(D, D, AAL_BF16, 1000000, 1, 8, 1.0f, 1.0f, DF, nullptr, nullptr, nullptr, AAL_BF16,
@@ -218,6 +228,7 @@ int main() {
   test_loss();
   test_grpo();
   test_vp();
+  test_stream_probe();
   test_noalloc();
   if (g_failures) {
     fprintf(stderr, "%d checks failed\n", g_failures);

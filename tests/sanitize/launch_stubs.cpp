@@ -79,4 +79,9 @@ hipError_t launch_vp_seq_scan(aal_vp_row_t*, const aal_vp_acc_t*, int32_t, int64
 }
 hipError_t launch_vp_grad(const VpSlice&, const aal_vp_row_t*, void*, DType) { ++g_stub_calls; return hipSuccess; }
 
+hipError_t launch_stream_probe(const void* const*, int, void*, size_t, uint32_t*, hipStream_t) {
+  ++g_stub_calls;
+  return hipSuccess;
+}
+
 }  // namespace aal
