@@ -377,3 +377,54 @@ def test_near_threshold_flags():
     assert not O.sim_near_threshold(zd, zt, 1.0, np.array([0.3]), np.array([0.3]))[0]
     # u2 right at min(1, p/q) = 1 is flagged
     assert O.sim_near_threshold(zd, zt, 1.0, np.array([0.3]), np.array([1.0 - 1e-7]))[0]
+
+
+# ------------------------------------------------- helpers pinned on their own
+def test_greedy_acceptance_is_draft_mass_on_target_argmax_by_hand():
+    """Eq. acc_greedy on a case worked by hand: target argmax is index 2, so
+    a = q(2) = e^1 / (e^0 + e^0 + e^1) for draft logits (0, 0, 1) at T = 1."""
+    zd = np.array([[0.0, 0.0, 1.0], [3.0, 0.0, 0.0]])
+    zt = np.array([[0.1, -2.0, 5.0], [-1.0, 4.0, 4.0]])
+    a, xs, q = O.acceptance_greedy(zd, zt, 1.0)
+    assert xs.tolist() == [2, 1]
+    e = np.e
+    np.testing.assert_allclose(a, [e / (2 + e), 1 / (e ** 3 + 2)], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(q.sum(-1), 1.0, atol=1e-15)
+
+
+def test_total_variation_by_hand_and_bounds():
+    """TV is half the l1 distance: 0 on equal rows, 1 on disjoint supports,
+    and 0.4 for (0.7, 0.3, 0) against (0.3, 0.3, 0.4)."""
+    p = np.array([[0.7, 0.3, 0.0], [1.0, 0.0, 0.0], [0.2, 0.5, 0.3]])
+    q = np.array([[0.3, 0.3, 0.4], [0.0, 0.5, 0.5], [0.2, 0.5, 0.3]])
+    np.testing.assert_allclose(O.total_variation(p, q), [0.4, 1.0, 0.0], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(O.total_variation(p, q), O.total_variation(q, p), atol=0)
+
+
+def test_survival_probabilities_by_hand():
+    """P(L >= k) for a = (1/2, 1/3, 3/4): 1/2, 1/6, 1/8; with a zero, every
+    later survival probability is zero."""
+    s = O.prob_accepted_at_least(np.array([[0.5, 1 / 3, 0.75], [0.9, 0.0, 1.0]]))
+    np.testing.assert_allclose(s, [[0.5, 1 / 6, 1 / 8], [0.9, 0.0, 0.0]], rtol=0, atol=1e-16)
+
+
+def test_grpo_windows_by_enumeration():
+    """Rows of each group's windows enumerated with plain loops: the windows
+    layout numbers rows group by group, window by window; the sequences layout
+    starts window j of group (b, g) at b*S + anchor[b, g] + j."""
+    w = O.grpo_windows(O.LAYOUT_WINDOWS, 2, 0, 3, 4)
+    r = 0
+    for g in range(2):
+        for j in range(3):
+            for k in range(4):
+                assert w[g, j, k] == r
+                r += 1
+    B, S, m, K = 2, 11, 3, 2
+    anchors = np.array([[0, 5], [2, 6]])
+    w = O.grpo_windows(O.LAYOUT_SEQUENCES, B, S, m, K, anchors)
+    assert w.shape == (4, m, K)
+    for b in range(B):
+        for g in range(2):
+            for j in range(m):
+                for k in range(K):
+                    assert w[b * 2 + g, j, k] == b * S + anchors[b, g] + j + k
