@@ -479,7 +479,13 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     };
     // Phase B (WTV) of rows [k0, k1): partial sums of min(p, q) and Q<,
     // reduced over the workgroup and published.
-    auto phase_b = [&](auto k0c, auto k1c) {
+    // hook(r) runs before the arithmetic of row k0 + r of the group (after
+    // that row's constants are read, so that LDS reads the hook issues do not
+    // hold it up) and, with r = KG, after the last row.  With the look-ahead
+    // (4-row first groups) every group's row constants are read before its
+    // first row (0.8% faster at K = 7, V = 128256); at K = 5 and 16 that
+    // raised the register count and measured slower.
+    auto phase_b = [&](auto k0c, auto k1c, auto hook) {
       constexpr int k0 = decltype(k0c)::value, k1 = decltype(k1c)::value, KG = k1 - k0;
       pin_all();
       float am[KG], aq[KG];
@@ -487,10 +493,26 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       // fma, log2 q = u - l2sd and log2 p = t - l2sd for dl = l2st - l2sd, so
       // min(p, q) = 2^-l2sd 2^min(u, t) and [q < p] = [u < t]: the common
       // factor is applied once per row after the reductions.
+      constexpr bool kPreload = kAhead;
+      float rmscd[kPreload ? KG : 1], rct[kPreload ? KG : 1];
+      if constexpr (kPreload) {
+#pragma unroll
+        for (int k = k0; k < k1; ++k) {
+          rmscd[k - k0] = sh_row[k][0];
+          rct[k - k0] = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
+        }
+      }
 #pragma unroll
       for (int k = k0; k < k1; ++k) {
-        const float mscd = sh_row[k][0];
-        const float ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
+        float mscd, ct;
+        if constexpr (kPreload) {
+          mscd = rmscd[k - k0];
+          ct = rct[k - k0];
+        } else {
+          mscd = sh_row[k][0];
+          ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
+        }
+        hook(k - k0);
         float sm = 0.f, sq = 0.f;
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
@@ -517,6 +539,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         am[k - k0] = sm;
         aq[k - k0] = sq;
       }
+      hook(KG);
       {
         constexpr int NP = (2 * KG + 3) / 4 * 4;
         float vv[NP], vt[NP / 4];
@@ -588,32 +611,46 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     } else if constexpr (K0 == K) {
       merge_a(0, K);
       lds_barrier();
-      phase_b(I0{}, IK{});
+      phase_b(I0{}, IK{}, [](int) {});
       merge_b(0, K);
       lds_barrier();
     } else {
       merge_a(0, K0);
       lds_barrier();
-      phase_b(I0{}, IK0{});
+      phase_b(I0{}, IK0{}, [](int) {});
       merge_a(K0, K);
       lds_barrier();
-      // The first group's target is dead: take the next window's staged
-      // copies into its registers, then restage the freed slots.
-      wait_vmem_all();  // this window's staging (issued in phase A) has landed
+      // The first group's target is dead: the next window's staged copies go
+      // to its registers, then the freed slots are restaged.
+      auto refill = [&]() {
+        wait_vmem_all();  // this window's staging (issued in phase A) has landed
 #pragma unroll
-      for (int i = 0; i < kFree; ++i) rt[i / NV][i % NV] = sh_pre_t[i][tid];
-      if (last) {
+        for (int i = 0; i < kFree; ++i) rt[i / NV][i % NV] = sh_pre_t[i][tid];
+      };
+      auto restage = [&]() {
+        if (last) {
 #pragma unroll
-        for (int k = 0; k < K0; ++k) mask_tail(rt, k);
+          for (int k = 0; k < K0; ++k) mask_tail(rt, k);
+        }
+        wait_lds_all();  // the slots are read before the loads below rewrite them
+#pragma unroll
+        for (int s = 0; s < kFree; ++s) {
+          const int i = kPre + (s < kUnst ? s : s - kUnst);
+          if (i < kPairs)
+            bld16_lds(s < kUnst ? nt : nd, &sh_pre_t[s][wbase], coff[i % NV], (i / NV) * p.row_bytes);
+        }
+      };
+      if constexpr (kAhead) {
+        // the reads land while the second group's first row is evaluated
+        phase_b(IK0{}, IK{}, [&](int r) {
+          if (r == 0) refill();
+          if (r == 1) restage();
+        });
+      } else {
+        refill();
+        restage();
+        phase_b(IK0{}, IK{}, [](int) {});
       }
-      wait_lds_all();  // the slots are read before the loads below rewrite them
-#pragma unroll
-      for (int s = 0; s < kFree; ++s) {
-        const int i = kPre + (s < kUnst ? s : s - kUnst);
-        if (i < kPairs)
-          bld16_lds(s < kUnst ? nt : nd, &sh_pre_t[s][wbase], coff[i % NV], (i / NV) * p.row_bytes);
-      }
-      phase_b(IK0{}, IK{});
       // the next window's first-group target partials, while the other
       // members' last partials are on their way (past the team's last window
       // the registers hold zeros and the results go unused)

@@ -569,7 +569,10 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
     };
     // Phase B of rows [k0, k1): the present sums (TV: sum min(p, q) and Q<;
     // KL), reduced over the workgroup and published.
-    auto phase_b = [&](auto k0c, auto k1c) {
+    // hook(r) runs before the arithmetic of row k0 + r of the group (after
+    // that row's constants are read, so that LDS reads the hook issues do not
+    // hold it up) and, with r = KG, after the last row.
+    auto phase_b = [&](auto k0c, auto k1c, auto hook) {
       constexpr int k0 = decltype(k0c)::value, k1 = decltype(k1c)::value, KG = k1 - k0;
       pin_all();
       float am[KG], aq[KG], ak[KG];
@@ -577,6 +580,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       for (int k = k0; k < k1; ++k) {
         const float mscd = sh_row[k][0];
         const float ct = sh_row[k][2] + (sh_row[k][3] - sh_row[k][1]);
+        hook(k - k0);
         float sm = 0.f, sq = 0.f, sk = 0.f;
 #pragma unroll
         for (int v = 0; v < NV; ++v) {
@@ -607,6 +611,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         aq[k - k0] = sq;
         ak[k - k0] = sk;
       }
+      hook(KG);
       {
         constexpr int C0 = TV ? 0 : 2;  // first component present
         constexpr int NC = (TV ? 2 : 0) + (KL ? 1 : 0);
@@ -697,20 +702,22 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
     } else if constexpr (K0 == K) {
       merge_a(0, K);
       lds_barrier();
-      phase_b(I0{}, IK{});
+      phase_b(I0{}, IK{}, [](int) {});
       merge_b(0, K);
     } else {
       merge_a(0, K0);
       lds_barrier();
-      phase_b(I0{}, IK0{});
+      phase_b(I0{}, IK0{}, [](int) {});
       merge_a(K0, K);
       lds_barrier();
-      if constexpr (kEarly) {
-        // the first group's target is dead: the next chunk's staged copies go
-        // to its registers, then the freed slots are restaged
+      // With kEarly the first group's target is dead: the next chunk's staged
+      // copies go to its registers, then the freed slots are restaged.
+      auto refill = [&]() {
         wait_vmem_all();  // this chunk's staging (issued in phase A) has landed
 #pragma unroll
         for (int i = 0; i < kFree; ++i) rt[i / NV][i % NV] = sh_pre[i][1][tid];
+      };
+      auto restage = [&]() {
         if (last) {
 #pragma unroll
           for (int k = 0; k < K0; ++k) mask_tail(rt, k);
@@ -722,8 +729,20 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           if (i < kPairs)
             bld16_lds(s < kUnst ? nt : nd, &sh_pre[s][1][wbase], coff[i % NV], (i / NV) * p.row_bytes);
         }
+      };
+      if constexpr (kAhead) {
+        // the reads land while the second group's first row is evaluated
+        phase_b(IK0{}, IK{}, [&](int r) {
+          if (r == 0) refill();
+          if (r == 1) restage();
+        });
+      } else {
+        if constexpr (kEarly) {
+          refill();
+          restage();
+        }
+        phase_b(IK0{}, IK{}, [](int) {});
       }
-      phase_b(IK0{}, IK{});
       if constexpr (kAhead) {
         // the next chunk's first-group target partials while the other
         // members' last partials are on their way (past the team's last chunk
