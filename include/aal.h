@@ -40,6 +40,17 @@
  * Workspace.  Device scratch of at least aal_workspace_bytes(rows, windows)
  *   bytes; its contents on entry are ignored and on exit unspecified.
  *   Concurrent calls must use distinct workspaces.
+ * Concurrency.  The register-resident schedule of the loss calls launches a
+ *   persistent grid no larger than the device holds at once, whose
+ *   workgroups wait for each other's partial results.  Other work on the
+ *   device can delay the placement of some of its workgroups, never prevent
+ *   it; but two resident launches that run at the same time (several streams
+ *   or processes on one device) could each hold part of the device while
+ *   waiting for the rest.  Calls on one stream never overlap.  Callers that
+ *   issue loss calls on several streams of one device at once pass
+ *   AAL_FLAG_COOPERATIVE, which leaves the placement of the whole grid to the
+ *   HIP runtime's cooperative launch.  Every wait is bounded: a wait that
+ *   times out (seconds) ends the kernel and the loss reads NaN.
  * Determinism.  No floating-point atomics: results are bitwise reproducible
  *   for a given device, shape and flags.
  */
@@ -73,6 +84,10 @@ typedef enum {
 
 /* Flags for the loss entry points (bitwise OR; 0 = automatic choice). */
 #define AAL_FLAG_STREAMING 1u /* force the multi-kernel streaming schedule            */
+/* Launch the register-resident kernel through the HIP runtime's cooperative
+ * launch, which places the whole grid before the kernel starts (see
+ * "Concurrency" above; it adds about 20 us per call). */
+#define AAL_FLAG_COOPERATIVE 2u
 
 /* Library version as major*10000 + minor*100 + patch. */
 int aal_version(void);

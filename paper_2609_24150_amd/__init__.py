@@ -7,6 +7,7 @@ include/aal.h); this package only marshals torch tensors to it.
 from .api import (  # noqa: F401
     AAL_BF16,
     AAL_F32,
+    AAL_FLAG_COOPERATIVE,
     AAL_FLAG_STREAMING,
     AAL_LAYOUT_SEQUENCES,
     AAL_LAYOUT_WINDOWS,

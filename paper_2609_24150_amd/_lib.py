@@ -19,6 +19,7 @@ AAL_ERR_ALIGN = 3
 AAL_ERR_WORKSPACE = 4
 AAL_ERR_HIP = 5
 AAL_FLAG_STREAMING = 1
+AAL_FLAG_COOPERATIVE = 2
 AAL_NOALLOC_SCRATCH_BYTES = 32 << 20
 AAL_LAYOUT_WINDOWS = 0
 AAL_LAYOUT_SEQUENCES = 1

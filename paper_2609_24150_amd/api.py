@@ -9,7 +9,8 @@ import torch
 
 from . import _lib
 from ._lib import (  # noqa: F401
-    AAL_BF16, AAL_F32, AAL_FLAG_STREAMING, AAL_LAYOUT_SEQUENCES, AAL_LAYOUT_WINDOWS, AAL_VP_EAL, AAL_VP_WTV,
+    AAL_BF16, AAL_F32, AAL_FLAG_COOPERATIVE, AAL_FLAG_STREAMING, AAL_LAYOUT_SEQUENCES, AAL_LAYOUT_WINDOWS,
+    AAL_VP_EAL, AAL_VP_WTV,
 )
 
 _DT = {torch.bfloat16: AAL_BF16, torch.float32: AAL_F32}

@@ -18,6 +18,8 @@ static __device__ __align__(256) uint8_t scratch[AAL_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
+constexpr uint32_t kKnownFlags = AAL_FLAG_STREAMING | AAL_FLAG_COOPERATIVE;
+
 // A plain per-thread buffer: nothing to construct or destroy at thread or
 // process exit.
 thread_local char g_last_error[512];
@@ -104,6 +106,7 @@ aal_status_t validate_common(const CommonIn& c) {
 }
 
 aal_status_t run_loss(aal::LossArgs& a, uint32_t flags) {
+  a.coop = (flags & AAL_FLAG_COOPERATIVE) != 0;
   bool used = false;
   hipError_t e = hipSuccess;
   if (!(flags & AAL_FLAG_STREAMING)) e = aal::launch_resident(a, &used);
@@ -211,7 +214,7 @@ aal_status_t eal_impl(const void* z_draft, const void* z_target, int in_dtype, i
   const float scd = scale_for(temp_draft);
   if (!positive_finite(temp_draft) || scd == 0.f)
     return fail(AAL_ERR_ARG, "temp_draft must be finite, > 0 and >= 1e-37");
-  if (flags & ~AAL_FLAG_STREAMING) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
+  if (flags & ~kKnownFlags) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
   aal::LossArgs a{};
   a.mode = aal::Mode::kEal;
   a.in = to_dtype(raw(in_dtype));
@@ -250,7 +253,7 @@ aal_status_t wtv_impl(const void* z_draft, const void* z_target, int in_dtype, i
     return fail(AAL_ERR_ARG, "temp_draft must be finite, > 0 and >= 1e-37");
   if (!positive_finite(temp_target) || sct == 0.f)
     return fail(AAL_ERR_ARG, "temp_target must be finite, > 0 and >= 1e-37");
-  if (flags & ~AAL_FLAG_STREAMING) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
+  if (flags & ~kKnownFlags) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
   aal::LossArgs a{};
   a.mode = aal::Mode::kWtv;
   a.in = to_dtype(raw(in_dtype));
@@ -434,7 +437,7 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
   };
   if (!finite(weights.wtv) || !finite(weights.eal) || !finite(weights.kl) || !finite(weights.tv))
     return fail(AAL_ERR_ARG, "weights must be finite");
-  if (flags & ~AAL_FLAG_STREAMING) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
+  if (flags & ~kKnownFlags) return fail(AAL_ERR_ARG, "unknown flags 0x%x", flags);
   const bool need_pq = weights.wtv != 0.f || weights.tv != 0.f || weights.kl != 0.f;
   const bool need_t = need_pq || (weights.eal != 0.f && labels == nullptr);
   if (!z_draft) return fail(AAL_ERR_ARG, "z_draft must be non-NULL");
@@ -502,6 +505,7 @@ aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const i
   wp += 256;
   a.loss_parts = reinterpret_cast<double*>(wp);
   a.streaming = (flags & AAL_FLAG_STREAMING) != 0;
+  a.coop = (flags & AAL_FLAG_COOPERATIVE) != 0;
   a.stream = stream;
   hipError_t e = aal::launch_general(a);
   if (e != hipSuccess) return fail(AAL_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));

@@ -74,6 +74,7 @@ struct LossArgs {
   void* grad;       // may be null
   const float* grad_scale;  // may be null
   Workspace ws;
+  bool coop;       // resident schedule: the runtime's cooperative launch
   hipStream_t stream;
 };
 
@@ -87,7 +88,8 @@ hipError_t launch_loss_reduce(const LossArgs& a, const unsigned* err = nullptr);
 
 // Register-resident single-kernel schedule.  Sets *used = false (and enqueues
 // nothing) when the shape is outside what it supports: V not a multiple of the 16-byte vector, K outside {1..8, 16}, a window too
-// wide for the co-resident grid, or no cooperative launch on the device.
+// wide for the co-resident grid, or (with a.coop) no cooperative launch on
+// the device.
 hipError_t launch_resident(const LossArgs& a, bool* used);
 
 // Per-row statistics of the combined-objective schedule.  64 bytes.
@@ -149,6 +151,7 @@ struct GenArgs {
   unsigned* res_err;       // workspace: poll time-out flag
   double* loss_parts;      // workspace [kGenLossParts][4]: first-stage sums of the loss
   bool streaming;          // force the multi-kernel schedule
+  bool coop;               // resident schedule: the runtime's cooperative launch
   hipStream_t stream;
 };
 

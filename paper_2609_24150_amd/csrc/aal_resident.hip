@@ -32,8 +32,11 @@
 // stage most of the next window's remaining pairs, so phase C issues few HBM
 // loads besides its gradient stores.
 //
-// The grid is persistent and launched cooperatively, so every member of a
-// team is resident.  Partials travel as 64-bit words {value, tag}: a reader
+// The grid is persistent and no larger than the device holds at once, so
+// every member of a team becomes resident (work already on the device can
+// delay the placement of some members, never prevent it; a launch through the
+// runtime's cooperative launch, on request, has the runtime place the whole
+// grid first, at about 20 us per call).  Partials travel as 64-bit words {value, tag}: a reader
 // polls the words it needs until every tag names the current window and
 // phase, so publishing doubles as the team barrier and no separate counter
 // round trip is needed.  Slots are double-buffered by window parity, which
@@ -872,7 +875,7 @@ hipError_t launch_k(const LossArgs& a, bool* used) {
   constexpr int kBlock = block_for<MODE>();
   auto kern = k_resident<TI, TG, MODE, K, NV, kBlock>;
   const DevInfo di = device_info();
-  if (!di.coop || di.cus == 0) return hipSuccess;
+  if ((a.coop && !di.coop) || di.cus == 0) return hipSuccess;
   const int ng = a.V / E;
   const int W = (ng + kBlock * NV - 1) / (kBlock * NV);
   const int64_t row_bytes = int64_t(a.V) * (a.in == DType::kBf16 ? 2 : 4);
@@ -915,9 +918,15 @@ hipError_t launch_k(const LossArgs& a, bool* used) {
   const int64_t nclear = words(T) + 1;
   k_clear<<<64, kClearBlock, 0, a.stream>>>(p.slots, nclear);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  void* args[] = {&p};
-  e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(unsigned(T * W)), dim3(kBlock), args, 0,
-                                 a.stream);
+  if (a.coop) {
+    void* args[] = {&p};
+    e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(unsigned(T * W)), dim3(kBlock), args, 0,
+                                   a.stream);
+  } else {
+    // the grid fits the device at once (see the occupancy bound above)
+    kern<<<dim3(unsigned(T * W)), dim3(kBlock), 0, a.stream>>>(p);
+    e = hipGetLastError();
+  }
   if (e != hipSuccess) return e;
   *used = true;
   return launch_loss_reduce(a, p.err);  // NaN loss if a poll timed out

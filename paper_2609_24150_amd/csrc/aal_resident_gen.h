@@ -1025,7 +1025,7 @@ hipError_t launch_kg(const GenArgs& a, bool* used) {
   constexpr int kBlock = kGenBlock;
   auto kern = k_res_gen<TI, TG, K, NV, VAR>;
   const DevInfo di = device_info();
-  if (!di.coop || di.cus == 0) return hipSuccess;
+  if ((a.coop && !di.coop) || di.cus == 0) return hipSuccess;
   const int ng = a.V / E;
   const int W = (ng + kBlock * NV - 1) / (kBlock * NV);
   const int64_t row_bytes = int64_t(a.V) * (a.in == DType::kBf16 ? 2 : 4);
@@ -1091,9 +1091,15 @@ hipError_t launch_kg(const GenArgs& a, bool* used) {
   if (CS > 1) k_gen_clear<<<256, kGenClearBlock, 0, a.stream>>>(p.arow, a.R * 2);
   k_gen_clear<<<1, 64, 0, a.stream>>>(reinterpret_cast<uint64_t*>(p.err), 1);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  void* args[] = {&p};
-  e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(unsigned(T * W)), dim3(kBlock), args, 0,
-                                 a.stream);
+  if (a.coop) {
+    void* args[] = {&p};
+    e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(unsigned(T * W)), dim3(kBlock), args, 0,
+                                   a.stream);
+  } else {
+    // the grid fits the device at once (see the occupancy bound above)
+    kern<<<dim3(unsigned(T * W)), dim3(kBlock), 0, a.stream>>>(p);
+    e = hipGetLastError();
+  }
   if (e != hipSuccess) return e;
   *used = true;
   return hipSuccess;

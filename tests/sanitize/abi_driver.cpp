@@ -72,7 +72,15 @@ static void test_eal_wtv() {
   EXPECT(aal_wtv_fwd_bwd_ex(D, D, AAL_BF16, N, K, V, 1.0f, 1.0f, DF, nullptr, nullptr, D, AAL_BF16, nullptr,
                             AAL_FLAG_STREAMING, ws, wb, nullptr),
          AAL_OK);
-  CHECK(aal::g_stub_calls == before + 4);
+  EXPECT(aal_wtv_fwd_bwd_ex(D, D, AAL_BF16, N, K, V, 1.0f, 1.0f, DF, nullptr, nullptr, D, AAL_BF16, nullptr,
+                            AAL_FLAG_COOPERATIVE, ws, wb, nullptr),
+         AAL_OK);
+  CHECK(aal::g_stub_calls == before + 5);
+  before = aal::g_stub_calls;
+  EXPECT(aal_wtv_fwd_bwd_ex(D, D, AAL_BF16, N, K, V, 1.0f, 1.0f, DF, nullptr, nullptr, D, AAL_BF16, nullptr, 4u, ws,
+                            wb, nullptr),
+         AAL_ERR_ARG);
+  CHECK(aal::g_stub_calls == before);
   // invalid arguments: nothing reaches a launcher
   before = aal::g_stub_calls;
   EXPECT(aal_eal_fwd_bwd(nullptr, D, AAL_BF16, N, K, V, 1.0f, DF, nullptr, nullptr, nullptr, nullptr, AAL_BF16,

@@ -53,6 +53,7 @@ aal_status_t (*f_sim)(const void*, const void*, aal_dtype_t, int32_t, int32_t, i
                       const float*, const float*, int32_t*, int32_t*, float*, float, int32_t, float,
                       void*, size_t, hipStream_t) = aal_sim_accept_grpo;
 _Static_assert(AAL_BF16 == 0 && AAL_F32 == 1, "dtype codes");
+_Static_assert(AAL_FLAG_STREAMING == 1u && AAL_FLAG_COOPERATIVE == 2u, "flag bits");
 _Static_assert(AAL_OK == 0 && AAL_ERR_ARG == 1 && AAL_ERR_DTYPE == 2 && AAL_ERR_ALIGN == 3 &&
                AAL_ERR_WORKSPACE == 4 && AAL_ERR_HIP == 5, "status codes");
 '''
@@ -128,7 +129,7 @@ def test_wtv_and_sim_validation(lib):
     assert st == 1 and b"temp_target" in L.aal_last_error()
     st = L.aal_wtv_fwd_bwd_ex(16, 16, 0, 2, 3, 8, 1.0, 1.0, 16, None, None, None, 0, None, 4, 256, 1 << 30, None)
     assert st == 1 and b"flags" in L.aal_last_error()
-    st = L.aal_eal_fwd_bwd_ex(16, 16, 0, 2, 3, 8, 1.0, 16, None, None, None, None, 0, None, 2, 256, 1 << 30, None)
+    st = L.aal_eal_fwd_bwd_ex(16, 16, 0, 2, 3, 8, 1.0, 16, None, None, None, None, 0, None, 4, 256, 1 << 30, None)
     assert st == 1 and b"flags" in L.aal_last_error()
     st = L.aal_eal_fwd_bwd_ex(16, 16, 0, 0, 3, 8, 1.0, 16, None, None, None, None, 0, None, 1, 256, 1 << 30, None)
     assert st == 1 and b"N must" in L.aal_last_error()
@@ -175,7 +176,7 @@ def _loss(L, lib, **kw):
     (dict(Td=0.0), 1), (dict(Tt=float("nan")), 1), (dict(w=(float("inf"), 0, 0, 0)), 1),
     (dict(zd=None), 1), (dict(zt=None), 1), (dict(zt=None, w=(0, 1.0, 0, 0)), 1), (dict(loss=None), 1),
     (dict(dt=5), 2), (dict(grad=16, gdt=7), 2), (dict(zd=20), 3), (dict(grad=40), 3),
-    (dict(ws=None), 4), (dict(ws=64), 3), (dict(wsb=1000), 4), (dict(B=1 << 30, S=4), 1), (dict(flags=2), 1),
+    (dict(ws=None), 4), (dict(ws=64), 3), (dict(wsb=1000), 4), (dict(B=1 << 30, S=4), 1), (dict(flags=4), 1),
 ])
 def test_loss_validation(lib, kw, code):
     L = lib.lib()
@@ -279,3 +280,8 @@ def test_vp_record_layouts_match_the_binding(tmp_path, lib):
     r = subprocess.run([cc, "-std=c11", "-fsyntax-only", f"-I{os.path.join(ROOT, 'include')}", str(src)],
                        capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def test_binding_flag_values_match_the_header(lib):
+    # the header's values are checked by the C compiler in the signature test
+    assert lib.AAL_FLAG_STREAMING == 1 and lib.AAL_FLAG_COOPERATIVE == 2

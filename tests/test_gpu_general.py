@@ -214,10 +214,12 @@ def test_resident_is_deterministic_and_agrees_with_streaming(A):
     w = (0.7, 0.4, 1.3, 0.9)
     r1 = A.aal_loss_fwd_bwd(zd, zt, 5, weights=w, layout=SEQ)
     r2 = A.aal_loss_fwd_bwd(zd, zt, 5, weights=w, layout=SEQ)
+    rc = A.aal_loss_fwd_bwd(zd, zt, 5, weights=w, layout=SEQ, flags=A.AAL_FLAG_COOPERATIVE)
     s = A.aal_loss_fwd_bwd(zd, zt, 5, weights=w, layout=SEQ, flags=1)
     torch.cuda.synchronize()
     for k in ("loss", "terms", "E_tv", "E_eal", "accept_tv", "accept_eal", "xstar", "grad"):
         assert torch.equal(r1[k], r2[k]), k
+        assert torch.equal(r1[k], rc[k]), k  # the cooperative launch: same grid, same bits
     assert rel_err(r1["loss"].item(), s["loss"].item()) < 1e-5
     assert torch.equal(r1["xstar"], s["xstar"])
     d = (r1["grad"].float() - s["grad"].float()).abs().max().item()

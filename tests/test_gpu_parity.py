@@ -224,6 +224,23 @@ def test_forward_only_and_stream_and_determinism(A, dev):
     assert torch.equal(e1["grad"], e2["grad"]) and torch.equal(e1["loss"], e2["loss"])
 
 
+@pytest.mark.parametrize("dtype,V,K,N", [(BF16, 128256, 7, 40), (BF16, 151936, 5, 30), (F32, 32000, 16, 20)])
+def test_cooperative_launch_gives_the_same_bits(A, dev, dtype, V, K, N):
+    """The resident kernel launched plainly (the default) and through the
+    runtime's cooperative launch (AAL_FLAG_COOPERATIVE): same grid, same bits,
+    and both agree with the oracle on a few windows."""
+    zd, zt = _inputs("c2", (N, K, V), dtype, seed=13, dev=dev)
+    for fn, args in ((A.aal_wtv_fwd_bwd, (0.9, 1.1)), (A.aal_eal_fwd_bwd, (0.8,))):
+        r0 = fn(zd, zt, *args, flags=0)
+        r1 = fn(zd, zt, *args, flags=A.AAL_FLAG_COOPERATIVE)
+        torch.cuda.synchronize()
+        for k in r0:
+            if r0[k] is not None:
+                assert torch.equal(r0[k], r1[k]), (fn.__name__, k)
+    _check_wtv(A, zd[:3], zt[:3], 0.9, 1.1, dtype, A.AAL_FLAG_COOPERATIVE)
+    _check_eal(A, zd[:3], zt[:3], 0.8, dtype, A.AAL_FLAG_COOPERATIVE)
+
+
 def test_boundary_errors_write_nothing(A, dev):
     from paper_2609_24150_amd import _lib
     zd, zt = _inputs("c2", (2, 3, 256), BF16, seed=1, dev=dev)
