@@ -143,8 +143,10 @@ aal_status_t aal_eal_fwd_bwd(const void* z_draft, const void* z_target, aal_dtyp
 
 /* aal_eal_fwd_bwd with schedule flags: flags = 0 is aal_eal_fwd_bwd;
  * AAL_FLAG_STREAMING forces the multi-kernel schedule (the same results
- * within the stated tolerances; used to cross-check the two schedules).
- * Unknown bits give AAL_ERR_ARG. */
+ * within the stated tolerances; used to cross-check the two schedules);
+ * AAL_FLAG_COOPERATIVE launches the resident kernel through the runtime's
+ * cooperative launch (the same bits; see "Concurrency").  Unknown bits give
+ * AAL_ERR_ARG. */
 aal_status_t aal_eal_fwd_bwd_ex(const void* z_draft, const void* z_target, aal_dtype_t in_dtype,
                                 int64_t N, int32_t K, int32_t V, float temp_draft,
                                 float* loss, float* eal_per_window, float* accept,
@@ -312,9 +314,9 @@ size_t aal_loss_workspace_bytes(aal_layout_t layout, int64_t B, int32_t S, int32
  * flags   : AAL_FLAG_* bits.  By default one register-resident kernel reads each
  *           logit once and writes the gradient once when V is a multiple of 8
  *           (bf16) / 4 (fp32), K is in {1..8, 16} and z_target is given; other
- *           shapes, and AAL_FLAG_STREAMING, take the multi-kernel schedule.  A
- *           poll time-out of the resident schedule (not expected) sets the loss
- *           to NaN.
+ *           shapes, and AAL_FLAG_STREAMING, take the multi-kernel schedule.
+ *           AAL_FLAG_COOPERATIVE: see "Concurrency".  A poll time-out of the
+ *           resident schedule (not expected) sets the loss to NaN.
  * workspace : at least aal_loss_workspace_bytes(layout, B, S, K) bytes.
  */
 aal_status_t aal_loss_fwd_bwd(const void* z_draft, const void* z_target, const int32_t* labels,
