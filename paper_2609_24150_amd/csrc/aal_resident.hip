@@ -107,8 +107,21 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
   // far as they go, its unstaged draft pairs: phase C, which carries the
   // gradient stores, is left with few or no HBM loads.
   constexpr int K0 = kWtv && K > 1 ? (K + 1) / 2 : K;
-  constexpr bool kEarly = kWtv && K0 < K && K0 * NV <= kPre;  // the first group is wholly staged
-  constexpr int kFree = kEarly ? K0 * NV : 0;                    // target slots refilled early
+  // EAL: the target is dead after phase A, so between publishing a window's
+  // partials and polling the team's, each wave takes the greedy token of the
+  // next window's wholly staged rows (up to 4) over its own columns: the
+  // largest value and its lowest index, the same fold as phase A, without
+  // the draft payload, which phase A then reads from the lane that holds it.
+#ifndef AAL_EAL_AHEAD
+#define AAL_EAL_AHEAD 1
+#endif
+  constexpr int kEA = (!kWtv && AAL_EAL_AHEAD) ? (kPre / NV < 4 ? (kPre / NV < K ? kPre / NV : K) : (K < 4 ? K : 4)) : 0;
+  constexpr int kEAPairs = kEA * NV;
+  // Target slots refilled early (WTV: the first row group after the second
+  // phase-A merge; EAL: the look-ahead rows before the merge); the freed
+  // slots then stage the next window's unstaged pairs.
+  constexpr bool kEarly = (kWtv && K0 < K && K0 * NV <= kPre) || (kEA > 0 && kPairs > kPre);
+  constexpr int kFree = kEarly ? (kWtv ? K0 * NV : kEAPairs) : 0;
   constexpr int kUnst = kPairs - kPre;                                 // unstaged pairs per tensor
   // Restaging slot of unstaged pair i (i >= kPre) of the target / draft, or
   // -1 when it still comes from HBM in phase C.
@@ -189,7 +202,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #ifndef AAL_AHEAD_MAX_ROWS
 #define AAL_AHEAD_MAX_ROWS 4
 #endif
-  constexpr bool kAhead = kEarly && K0 >= AAL_AHEAD_MIN_ROWS && K0 <= AAL_AHEAD_MAX_ROWS;
+  constexpr bool kAhead = kWtv && kEarly && K0 >= AAL_AHEAD_MIN_ROWS && K0 <= AAL_AHEAD_MAX_ROWS;
   constexpr int KE = kAhead ? K0 : 1;
   float em[KE], es[KE];
   auto target_partial = [&](int k, float& mo, float& so) {
@@ -221,6 +234,55 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
     for (int v = 0; v < NV; ++v)
       if (col[v] >= p.ng) r[k][v] = neg_inf_vec(TI{});
+  };
+
+  // EAL look-ahead (see kEA above): per row the wave's largest target value,
+  // its lowest index and the lane holding it
+  constexpr int kEAR = kEA > 0 ? kEA : 1;
+  float eab[kEAR];
+  int eax[kEAR], eas[kEAR];
+  auto argmax_ahead = [&](int k, float& bo, int& xo, int& so) {
+    float xs[NV][E];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
+    float best = kNegInf;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < E; ++e) best = fmaxf(best, xs[v][e]);
+    int li = 0;
+#pragma unroll
+    for (int v = NV - 1; v >= 0; --v)
+#pragma unroll
+      for (int e = E - 1; e >= 0; --e)
+        if (xs[v][e] == best) li = v * E + e;
+    const int idx = best == kNegInf ? INT_MAX : col[0] * E + (li / E) * (kBlock * E) + li % E;
+    float m[1] = {best};
+    wave_max_n(m);
+    const int x = wave_min_i(best == m[0] ? idx : INT_MAX);
+    const uint64_t own = __builtin_amdgcn_ballot_w64(best == m[0] && idx == x);
+    bo = m[0];
+    xo = x;
+    so = own != 0 ? __builtin_ctzll(own) : 0;
+  };
+  // the draft logit at element x of row k (wave-uniform x, held by lane src)
+  auto payload = [&](int k, int x, int src) {
+    if (x == INT_MAX) return kNegInf;
+    const int c = x / E - member * (kBlock * NV);
+    const int vv = c / kBlock, e = x % E;
+    constexpr int EPW = E / 4;
+    const int q = e / EPW;
+    uint32_t wd = 0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq)
+        if (v == vv && qq == q) wd = __builtin_amdgcn_readlane(rd[k][v][qq], src);
+    if constexpr (EPW == 2) {
+      return __builtin_bit_cast(float, (e & 1) ? (wd & 0xffff0000u) : (wd << 16));
+    } else {
+      return __builtin_bit_cast(float, wd);
+    }
   };
 
   int64_t w = team;
@@ -257,6 +319,13 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         target_partial(k, em[k], es[k]);
       }
     }
+    if constexpr (kEA > 0) {
+#pragma unroll
+      for (int k = 0; k < kEA; ++k) {
+        if (last) mask_tail(rt, k);
+        argmax_ahead(k, eab[k], eax[k], eas[k]);
+      }
+    }
   }
   // read once: a global load inside the scan would sit on every window's
   // critical path
@@ -286,6 +355,17 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           bld16_lds(nd, &sh_pre_d[i][wbase], coff[v], k * p.row_bytes);
           bld16_lds(nt, &sh_pre_t[i][wbase], coff[v], k * p.row_bytes);
         }
+      }
+    };
+    // The kFree target slots refilled early stage the next window's unstaged
+    // pairs: its targets first, then as many of its drafts as remain.
+    auto restage_freed = [&]() {
+      wait_lds_all();  // the slots are read before the loads below rewrite them
+#pragma unroll
+      for (int s = 0; s < kFree; ++s) {
+        const int i = kPre + (s < kUnst ? s : s - kUnst);
+        if (i < kPairs)
+          bld16_lds(s < kUnst ? nt : nd, &sh_pre_t[s][wbase], coff[i % NV], (i / NV) * p.row_bytes);
       }
     };
 
@@ -338,6 +418,10 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
           } else {
             target_partial(k, m1[k], s1[k]);
           }
+        } else if (k < kEA) {  // evaluated during the previous window's merge
+          m1[k] = eab[k < kEAR ? k : 0];
+          s1[k] = __builtin_bit_cast(float, eax[k < kEAR ? k : 0]);
+          z1[k] = payload(k, eax[k < kEAR ? k : 0], eas[k < kEAR ? k : 0]);
         } else {
 #pragma unroll
           for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
@@ -609,8 +693,21 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 
     // ------------------------------------------------------------ phase B
     if constexpr (!kWtv) {
+      if constexpr (kEA > 0) {
+        wait_vmem_all();  // the next window's staging (issued in phase A) has landed
+#pragma unroll
+        for (int i = 0; i < kEAPairs; ++i) rt[i / NV][i % NV] = sh_pre_t[i][tid];
+#pragma unroll
+        for (int k = 0; k < kEA; ++k) {
+          if (last) mask_tail(rt, k);
+          argmax_ahead(k, eab[k], eax[k], eas[k]);
+        }
+      }
       merge_a(0, K);
       lds_barrier();
+      // issued after the polls, which would otherwise wait for these loads
+      // (vector-memory instructions complete in issue order)
+      if constexpr (kEarly) restage_freed();
     } else if constexpr (K0 == K) {
       merge_a(0, K);
       lds_barrier();
@@ -635,13 +732,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
           for (int k = 0; k < K0; ++k) mask_tail(rt, k);
         }
-        wait_lds_all();  // the slots are read before the loads below rewrite them
-#pragma unroll
-        for (int s = 0; s < kFree; ++s) {
-          const int i = kPre + (s < kUnst ? s : s - kUnst);
-          if (i < kPairs)
-            bld16_lds(s < kUnst ? nt : nd, &sh_pre_t[s][wbase], coff[i % NV], (i / NV) * p.row_bytes);
-        }
+        restage_freed();
       };
       if constexpr (kAhead) {
         // the reads land while the second group's first row is evaluated
@@ -806,9 +897,10 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       asm volatile("" ::: "memory");  // keep the refill below this slot's store
       if (i < kPre) {
         rd[k][v] = sh_pre_d[i][tid];
-        // target pairs below kFree were refilled after merge A; with restaging
-        // the others are read after the wait above
-        if (!kEarly) rt[k][v] = sh_pre_t[i][tid];
+        // target pairs below kFree were refilled after merge A (EAL: below
+        // kEAPairs, before it); with restaging the others are read after the
+        // wait above
+        if (!kEarly && i >= kEAPairs) rt[k][v] = sh_pre_t[i][tid];
       } else {
         const int sd = kEarly ? rslot_d(i) : -1, st = kEarly ? rslot_t(i) : -1;
         rd[k][v] = sd >= 0 ? sh_pre_t[sd][tid] : bld16(nd, coff[v], k * p.row_bytes);
