@@ -241,6 +241,12 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
   constexpr int kEAR = kEA > 0 ? kEA : 1;
   float eab[kEAR];
   int eax[kEAR], eas[kEAR];
+  // and, once those registers are free again, the same rows' draft (max,
+  // sum-exp) partials from the draft's staged copies: with 4 such rows
+  // (K = 7: 1.7% faster); with 3 (K = 5, 13-member teams) it measured 2%
+  // slower
+  constexpr bool kEAD = kEA >= 4;
+  float edm[kEAR], eds[kEAR];
   auto argmax_ahead = [&](int k, float& bo, int& xo, int& so) {
     float xs[NV][E];
 #pragma unroll
@@ -264,6 +270,31 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     bo = m[0];
     xo = x;
     so = own != 0 ? __builtin_ctzll(own) : 0;
+  };
+  // the draft's (max, sum-exp) partial of row k from registers r, as phase A
+  // evaluates it
+  auto draft_partial = [&](const u32x4 (&r)[K][NV], int k, float& mo, float& so) {
+    float xs[NV][E];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) unpackv<TI, E>(r[k][v], xs[v]);
+    float m = kNegInf;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < E; ++e) m = fmaxf(m, xs[v][e]);
+    const float msc = m * p.scd;
+    float sum = 0.f;
+    if (m != kNegInf) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const float x = ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
+          sum = (v == 0 && e == 0) ? x : sum + x;  // no add of the initial zero
+        }
+    }
+    mo = m == kNegInf ? kNegInf : msc;
+    so = sum;
   };
   // the draft logit at element x of row k (wave-uniform x, held by lane src)
   auto payload = [&](int k, int x, int src) {
@@ -322,8 +353,12 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
     if constexpr (kEA > 0) {
 #pragma unroll
       for (int k = 0; k < kEA; ++k) {
-        if (last) mask_tail(rt, k);
+        if (last) {
+          mask_tail(rt, k);
+          mask_tail(rd, k);
+        }
         argmax_ahead(k, eab[k], eax[k], eas[k]);
+        if constexpr (kEAD) draft_partial(rd, k, edm[k], eds[k]);
       }
     }
   }
@@ -391,26 +426,12 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       for (int k = k0; k < k1; ++k) {
         stage_row(k);  // issued between the rows' arithmetic, the loads do not stall the wave
         float xs[NV][E];
-#pragma unroll
-        for (int v = 0; v < NV; ++v) unpackv<TI, E>(rd[k][v], xs[v]);
-        float m = kNegInf;
-#pragma unroll
-        for (int v = 0; v < NV; ++v)
-#pragma unroll
-          for (int e = 0; e < E; ++e) m = fmaxf(m, xs[v][e]);
-        const float msc = m * p.scd;
-        float sum = 0.f;
-        if (m != kNegInf) {
-#pragma unroll
-          for (int v = 0; v < NV; ++v)
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-              const float x = ex2(__builtin_fmaf(xs[v][e], p.scd, -msc));
-              sum = (v == 0 && e == 0) ? x : sum + x;  // no add of the initial zero
-            }
+        if (kEAD && k < kEA) {  // evaluated during the previous window's merge
+          m0[k] = edm[k < kEAR ? k : 0];
+          s0[k] = eds[k < kEAR ? k : 0];
+        } else {
+          draft_partial(rd, k, m0[k], s0[k]);
         }
-        m0[k] = m == kNegInf ? kNegInf : msc;
-        s0[k] = sum;
         if constexpr (kWtv) {
           if (kAhead && k < K0) {  // evaluated during the previous window's last merge
             m1[k] = em[k < KE ? k : 0];
@@ -701,6 +722,17 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         for (int k = 0; k < kEA; ++k) {
           if (last) mask_tail(rt, k);
           argmax_ahead(k, eab[k], eax[k], eas[k]);
+        }
+        if constexpr (kEAD) {
+          // the target registers of these rows are free again: the next
+          // window's staged draft copies, for its draft partials
+#pragma unroll
+          for (int i = 0; i < kEAPairs; ++i) rt[i / NV][i % NV] = sh_pre_d[i][tid];
+#pragma unroll
+          for (int k = 0; k < kEA; ++k) {
+            if (last) mask_tail(rt, k);
+            draft_partial(rt, k, edm[k], eds[k]);
+          }
         }
       }
       merge_a(0, K);
