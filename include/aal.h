@@ -25,7 +25,8 @@
  *   frees, or keeps a pointer past the call.
  * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Every
  *   call only enqueues kernels on it and returns; results are valid once the stream has been synchronised.  No call synchronises the
- *   host.
+ *   host.  Nothing else is enqueued (no memset or copy nodes), so with the
+ *   default flags a call can be captured into a HIP graph and replayed.
  * Layout.  Logits are contiguous row-major [N, K, V] (simulation: [P, G, K, V]);
  *   row r = n*K + k holds position k of window n; the row stride is V elements.
  *   Element offsets are 64-bit.
