@@ -51,7 +51,9 @@
  *   issue loss calls on several streams of one device at once pass
  *   AAL_FLAG_COOPERATIVE, which leaves the placement of the whole grid to the
  *   HIP runtime's cooperative launch.  Every wait is bounded: a wait that
- *   times out (seconds) ends the kernel and the loss reads NaN.
+ *   times out (seconds) ends the kernel and the loss reads NaN.  With the
+ *   environment variable AAL_TEST_PRESET_TIMEOUT=1 the resident kernels start
+ *   in that state (a test hook for the time-out path).
  * Determinism.  No floating-point atomics: results are bitwise reproducible
  *   for a given device, shape and flags.
  */

@@ -972,9 +972,10 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 }
 
 // Zeroes the tag words (tag 0 never matches) and the error word.
-__global__ void k_clear(uint64_t* p, int64_t n) {
+// Zeroes the slot words p[0 .. n-2]; the error word p[n-1] takes `err`.
+__global__ void k_clear(uint64_t* p, int64_t n, uint64_t err) {
   for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
-    p[i] = 0;
+    p[i] = i == n - 1 ? err : 0;
 }
 
 // -------------------------------------------------------------- dispatch
@@ -1040,7 +1041,7 @@ hipError_t launch_k(const LossArgs& a, bool* used) {
   p.slots = reinterpret_cast<uint64_t*>(a.ws.resident);
   p.err = reinterpret_cast<unsigned*>(p.slots + words(T));
   const int64_t nclear = words(T) + 1;
-  k_clear<<<64, kClearBlock, 0, a.stream>>>(p.slots, nclear);
+  k_clear<<<64, kClearBlock, 0, a.stream>>>(p.slots, nclear, initial_error_word());
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (a.coop) {
     void* args[] = {&p};

@@ -7,6 +7,8 @@
 
 #include <limits.h>
 
+#include <stdlib.h>
+
 #include <atomic>
 
 namespace aal {
@@ -237,6 +239,16 @@ __device__ __forceinline__ void wave_argmax(float& bv, float& bi, float& bz) {
   bz = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bz), src));
   bv = m[0];
   bi = __builtin_bit_cast(float, x);
+}
+
+// The value the resident kernels' error word starts at: 0, or 1 when the
+// environment variable AAL_TEST_PRESET_TIMEOUT is "1" — the state a poll
+// time-out leaves, so that tests can drive the time-out path (every bounded
+// wait then ends at once, the kernel drains and the loss reads NaN) without
+// waiting seconds for a real one.
+inline uint64_t initial_error_word() {
+  const char* v = getenv("AAL_TEST_PRESET_TIMEOUT");
+  return (v != nullptr && v[0] == '1' && v[1] == '\0') ? 1u : 0u;
 }
 
 struct DevInfo {

@@ -1013,14 +1013,15 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   wait_vmem_all();
 }
 
-// Zeroes the slot words, the acceptance words of windows sliding over
-// sequences (n1 = 0 without) and the error word, in one launch.
-__global__ void k_gen_clear(uint64_t* p0, int64_t n0, uint64_t* p1, int64_t n1, uint64_t* err_word) {
+// Zeroes the slot words and the acceptance words of windows sliding over
+// sequences (n1 = 0 without), and sets the error word to `err`, in one launch.
+__global__ void k_gen_clear(uint64_t* p0, int64_t n0, uint64_t* p1, int64_t n1, uint64_t* err_word,
+                            uint64_t err) {
   const int64_t stride = int64_t(gridDim.x) * blockDim.x;
   const int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   for (int64_t i = t; i < n0; i += stride) p0[i] = 0;
   for (int64_t i = t; i < n1; i += stride) p1[i] = 0;
-  if (t == 0) *err_word = 0;
+  if (t == 0) *err_word = err;
 }
 
 template <class TI, class TG, int K, int VAR>
@@ -1093,7 +1094,8 @@ hipError_t launch_kg(const GenArgs& a, bool* used) {
   p.arow = a.arow;
   p.err = a.res_err;
   k_gen_clear<<<CS > 1 ? 256 : 64, kGenClearBlock, 0, a.stream>>>(p.slots, words(T), p.arow, CS > 1 ? a.R * 2 : 0,
-                                                                  reinterpret_cast<uint64_t*>(p.err));
+                                                                  reinterpret_cast<uint64_t*>(p.err),
+                                                                  initial_error_word());
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (a.coop) {
     void* args[] = {&p};
