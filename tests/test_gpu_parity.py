@@ -72,7 +72,10 @@ SHAPES = [(1, 1, 3), (2, 2, 3), (3, 7, 2), (7, 3, 3), (8, 4, 2), (9, 2, 3), (102
           # K = 6 and 8 on teams of several members: the fused WTV schedule splits their
           # unstaged pairs differently (at K = 6 every unstaged draft pair is restaged; at
           # K = 8 the first row group's target partials are evaluated one window ahead)
-          (20000, 6, 3), (32000, 8, 2)]
+          (20000, 6, 3), (32000, 8, 2),
+          # window lengths the resident kernel does not take (the streaming schedule
+          # runs them in both paths), up to the largest K the boundary accepts
+          (3000, 12, 2), (1000, 64, 2)]
 
 
 @pytest.mark.parametrize("path", ["auto", "stream"])
