@@ -60,11 +60,14 @@ def _cpu_worker(args):
     n = 0
     t0 = time.perf_counter()
     while True:
-        O.wtv_loss(zd, zt, Td, Tt)
+        o = O.wtv_loss(zd, zt, Td, Tt)
         n += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
-            return n * nwin * K, el
+            # the last evaluation, kept for the parity sample of the GPU results
+            res = {"loss": float(o["loss"]), "E": np.asarray(o["E"]), "a": np.asarray(o["a"]),
+                   "grad": np.asarray(o["grad"], dtype=np.float32)}
+            return n * nwin * K, el, res
 
 
 def cpu_baseline(workload: str, budget_s: float = 12.0) -> dict:
@@ -86,11 +89,49 @@ def cpu_baseline(workload: str, budget_s: float = 12.0) -> dict:
     rows = sum(r[0] for r in res)
     # each worker's rate over its own timed loop, summed: the aggregate rate
     rate = sum(r[0] / r[1] for r in res)
+    _ORACLE_SAMPLES[:] = [(1000 + w, nwin, r[2]) for w, r in enumerate(res)]
     return {"value": rate, "unit": "logit rows/s", "cores": workers, "kind": "oracle",
             "sample": f"{workers} processes x {nwin} windows of the workload (K={K}, V={V}), each repeated "
                       f"for ~{budget_s:.0f}s; {rows} rows in {wall:.1f}s wall",
             "rows_per_s_per_core": rate / workers, "affinity_cores": cores,
             "worker_cap": f"{HOST_CPU_SHARE} (the host CPU share of one GPU)", "cpu_model": _cpu_model()}
+
+
+# (seed, windows, oracle result) of each CPU worker's input: the oracle's own
+# results, compared after the timed legs with the library's on the same inputs
+_ORACLE_SAMPLES = []
+
+
+def parity_sample(workload: str) -> dict:
+    """The library's WTV call on each CPU worker's seeded windows against the
+    oracle's results for them (computed in the CPU leg): the largest relative
+    error of the loss and of E, the largest absolute error of the acceptances,
+    and the largest gradient error relative to the largest gradient entry.
+    Reported, not asserted (the parity tests assert the stated tolerances)."""
+    import numpy as np
+    import torch
+
+    import paper_2609_24150_amd as A
+    from paper_2609_24150_amd.inputs import CONFIGS, make_logits
+    cfg = CONFIGS[workload]
+    K, V = cfg["K"], cfg["V"]
+    worst = {"loss_rel": 0.0, "E_rel": 0.0, "accept_abs": 0.0, "grad_abs_over_max": 0.0}
+    n = 0
+    for seed, nwin, o in _ORACLE_SAMPLES:
+        zd, zt = make_logits(cfg["recipe"], (nwin, K, V), cfg["dtype"], seed=seed, device="cpu")
+        r = A.aal_wtv_fwd_bwd(zd.cuda(), zt.cuda(), cfg["temp_draft"], cfg["temp_target"], grad_dtype=cfg["dtype"])
+        torch.cuda.synchronize()
+        rel = lambda a, b: float(np.max(np.abs(a - b) / np.maximum(np.abs(b), 1e-30)))  # noqa: E731
+        worst["loss_rel"] = max(worst["loss_rel"], rel(np.float64(r["loss"].item()), np.float64(o["loss"])))
+        worst["E_rel"] = max(worst["E_rel"], rel(r["E"].cpu().double().numpy(), o["E"]))
+        worst["accept_abs"] = max(worst["accept_abs"],
+                                  float(np.max(np.abs(r["accept"].cpu().double().numpy() - o["a"]))))
+        g = r["grad"].cpu().float().numpy()
+        worst["grad_abs_over_max"] = max(worst["grad_abs_over_max"],
+                                         float(np.max(np.abs(g - o["grad"])) / np.max(np.abs(o["grad"]))))
+        n += nwin
+        del r, zd, zt
+    return {"windows": n, **worst, "inputs": "each CPU worker's seeded windows of the workload"}
 
 
 def _cpu_model() -> str:
@@ -587,6 +628,9 @@ def main():
             if "alg_GBps" in leg and "frac" not in leg:
                 leg["frac"] = leg["alg_GBps"] / HBM_PEAK_GBPS
         out["also"] = also
+    if cpu is not None and _ORACLE_SAMPLES:
+        _progress("parity sample against the CPU leg's oracle results")
+        cpu["parity_sample"] = parity_sample(args.workload)
     print(json.dumps(out))
 
 
