@@ -203,6 +203,11 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #define AAL_AHEAD_MAX_ROWS 4
 #endif
   constexpr bool kAhead = kWtv && kEarly && K0 >= AAL_AHEAD_MIN_ROWS && K0 <= AAL_AHEAD_MAX_ROWS;
+  // Cache policy of the logit loads and gradient stores: nontemporal, except
+  // for WTV with the look-ahead, whose ordinary cached accesses measured 1%
+  // faster at K = 7, V = 128256 (nontemporal is faster for EAL, by 2-5%, and
+  // for WTV at K = 5 and 16, by 1-2%).
+  constexpr int kCp = kAhead ? 0 : kNontemporal;
   constexpr int KE = kAhead ? K0 : 1;
   float em[KE], es[KE];
   auto target_partial = [&](int k, float& mo, float& so) {
@@ -326,14 +331,14 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
       const int k = i / NV, v = i % NV;
-      bld16_lds(bd, &sh_pre_d[i][wbase], coff[v], k * p.row_bytes);
-      bld16_lds(bt, &sh_pre_t[i][wbase], coff[v], k * p.row_bytes);
+      bld16_lds<kCp>(bd, &sh_pre_d[i][wbase], coff[v], k * p.row_bytes);
+      bld16_lds<kCp>(bt, &sh_pre_t[i][wbase], coff[v], k * p.row_bytes);
     }
 #pragma unroll
     for (int i = kPre; i < kPairs; ++i) {
       const int k = i / NV, v = i % NV;
-      rd[k][v] = bld16(bd, coff[v], k * p.row_bytes);
-      rt[k][v] = bld16(bt, coff[v], k * p.row_bytes);
+      rd[k][v] = bld16<kCp>(bd, coff[v], k * p.row_bytes);
+      rt[k][v] = bld16<kCp>(bt, coff[v], k * p.row_bytes);
     }
     wait_vmem_all();
 #pragma unroll
@@ -387,8 +392,8 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       for (int v = 0; v < NV; ++v) {
         const int i = k * NV + v;
         if (i < kPre) {
-          bld16_lds(nd, &sh_pre_d[i][wbase], coff[v], k * p.row_bytes);
-          bld16_lds(nt, &sh_pre_t[i][wbase], coff[v], k * p.row_bytes);
+          bld16_lds<kCp>(nd, &sh_pre_d[i][wbase], coff[v], k * p.row_bytes);
+          bld16_lds<kCp>(nt, &sh_pre_t[i][wbase], coff[v], k * p.row_bytes);
         }
       }
     };
@@ -400,7 +405,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
       for (int s = 0; s < kFree; ++s) {
         const int i = kPre + (s < kUnst ? s : s - kUnst);
         if (i < kPairs)
-          bld16_lds(s < kUnst ? nt : nd, &sh_pre_t[s][wbase], coff[i % NV], (i / NV) * p.row_bytes);
+          bld16_lds<kCp>(s < kUnst ? nt : nd, &sh_pre_t[s][wbase], coff[i % NV], (i / NV) * p.row_bytes);
       }
     };
 
@@ -925,7 +930,7 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
 #pragma unroll
         for (int e = 0; e < E; ++e) g[e] = cA * ex2(__builtin_fmaf(xd[e], p.scd, -mscd));
       }
-      store_g<TG, E>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
+      store_g<TG, E, kCp>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
       asm volatile("" ::: "memory");  // keep the refill below this slot's store
       if (i < kPre) {
         rd[k][v] = sh_pre_d[i][tid];
@@ -935,9 +940,9 @@ __global__ __launch_bounds__(kBlock) void k_resident(ResParams p) {
         if (!kEarly && i >= kEAPairs) rt[k][v] = sh_pre_t[i][tid];
       } else {
         const int sd = kEarly ? rslot_d(i) : -1, st = kEarly ? rslot_t(i) : -1;
-        rd[k][v] = sd >= 0 ? sh_pre_t[sd][tid] : bld16(nd, coff[v], k * p.row_bytes);
+        rd[k][v] = sd >= 0 ? sh_pre_t[sd][tid] : bld16<kCp>(nd, coff[v], k * p.row_bytes);
         if (st < 0) {
-          rt[k][v] = bld16(nt, coff[v], k * p.row_bytes);
+          rt[k][v] = bld16<kCp>(nt, coff[v], k * p.row_bytes);
         } else if (j >= kC0 + kPre) {  // C2 (a C0 pair's restaged target is read after the wait)
           rt[k][v] = sh_pre_t[st][tid];
         }

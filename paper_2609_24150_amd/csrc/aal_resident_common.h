@@ -34,14 +34,17 @@ constexpr int kNontemporal = 2;
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), int(bytes), kRawBufferWord3);
 }
+// CP: the cache-policy bits of the access (nontemporal by default)
+template <int CP = kNontemporal>
 __device__ __forceinline__ u32x4 bld16(rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kNontemporal);
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, CP);
 }
 // The same 16 bytes per lane, delivered straight to LDS: lane l of the wave
 // writes bytes [16 l, 16 l + 16) from `dst` (wave-uniform), no VGPRs involved.
 typedef __attribute__((address_space(3))) void lds_void_t;
+template <int CP = kNontemporal>
 __device__ __forceinline__ void bld16_lds(rsrc_t r, void* dst, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)dst, 16, voff, soff, 0, kNontemporal);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)dst, 16, voff, soff, 0, CP);
 }
 // s_waitcnt vmcnt(0) as an instruction the compiler's wait-count tracking sees
 // (gfx9 encoding: vmcnt 0, expcnt 7, lgkmcnt 15).
@@ -66,26 +69,26 @@ __device__ __forceinline__ void wait_lds_all() { __builtin_amdgcn_s_waitcnt(0xC0
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // One vector of gradient values at per-lane byte offset `off` of a row.
-template <class TG, int E>
+template <class TG, int E, int CP = kNontemporal>
 __device__ __forceinline__ void store_g(rsrc_t r, uint32_t off, const float (&g)[E]) {
   if constexpr (sizeof(typename TG::storage) == 2 && E == 8) {
     const u32x4 w = {pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]), pack_bf16x2(g[4], g[5]),
                      pack_bf16x2(g[6], g[7])};
-    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, kNontemporal);
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, CP);
   } else if constexpr (sizeof(typename TG::storage) == 2 && E == 4) {
     const u32x2 w = {pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])};
-    __builtin_amdgcn_raw_buffer_store_b64(w, r, off, 0, kNontemporal);
+    __builtin_amdgcn_raw_buffer_store_b64(w, r, off, 0, CP);
   } else if constexpr (E == 4) {
     const u32x4 w = {__builtin_bit_cast(uint32_t, g[0]), __builtin_bit_cast(uint32_t, g[1]),
                      __builtin_bit_cast(uint32_t, g[2]), __builtin_bit_cast(uint32_t, g[3])};
-    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, kNontemporal);
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, CP);
   } else {
     const u32x4 w0 = {__builtin_bit_cast(uint32_t, g[0]), __builtin_bit_cast(uint32_t, g[1]),
                       __builtin_bit_cast(uint32_t, g[2]), __builtin_bit_cast(uint32_t, g[3])};
     const u32x4 w1 = {__builtin_bit_cast(uint32_t, g[4]), __builtin_bit_cast(uint32_t, g[5]),
                       __builtin_bit_cast(uint32_t, g[6]), __builtin_bit_cast(uint32_t, g[7])};
-    __builtin_amdgcn_raw_buffer_store_b128(w0, r, off, 0, kNontemporal);
-    __builtin_amdgcn_raw_buffer_store_b128(w1, r, off + 16u, 0, kNontemporal);
+    __builtin_amdgcn_raw_buffer_store_b128(w0, r, off, 0, CP);
+    __builtin_amdgcn_raw_buffer_store_b128(w1, r, off + 16u, 0, CP);
   }
 }
 
