@@ -134,6 +134,11 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   // data), the first group's target partials of a chunk are evaluated during
   // the previous chunk's last team merge, with a first group of 4 rows.
   constexpr bool kAhead = kEarly && !AM && K0 == 4;
+  // Cache policy of the logit loads and gradient stores: ordinary cached
+  // accesses for the look-ahead variants (sliding WTV over 7 x 2048 rows of
+  // V = 128256 0.8% faster than nontemporal ones; disjoint windows 1% slower,
+  // a case the fused EAL/WTV kernel serves), nontemporal otherwise.
+  constexpr int kCp = kAhead ? 0 : kNontemporal;
   constexpr int KE = kAhead ? K0 : 1;
   constexpr int kPairsPerReg = 32 / E;
   constexpr int kMaskRegs = MB ? (kPairs + kPairsPerReg - 1) / kPairsPerReg : 1;
@@ -247,14 +252,14 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
       const int k = i / NV, v = i % NV;
-      bld16_lds(bd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
-      bld16_lds(bt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+      bld16_lds<kCp>(bd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
+      bld16_lds<kCp>(bt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
     }
 #pragma unroll
     for (int i = kPre; i < kPairs; ++i) {
       const int k = i / NV, v = i % NV;
-      rd[k][v] = bld16(bd, coff[v], k * p.row_bytes);
-      rt[k][v] = bld16(bt, coff[v], k * p.row_bytes);
+      rd[k][v] = bld16<kCp>(bd, coff[v], k * p.row_bytes);
+      rt[k][v] = bld16<kCp>(bt, coff[v], k * p.row_bytes);
     }
     wait_vmem_all();
 #pragma unroll
@@ -333,8 +338,8 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         for (int v = 0; v < NV; ++v) {
           const int i = k * NV + v;
           if (i < kPre) {
-            bld16_lds(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
-            bld16_lds(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
+            bld16_lds<kCp>(nd, &sh_pre[i][0][wbase], coff[v], k * p.row_bytes);
+            bld16_lds<kCp>(nt, &sh_pre[i][1][wbase], coff[v], k * p.row_bytes);
           }
         }
         float xs[NV][E];
@@ -727,7 +732,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         for (int s = 0; s < kFree; ++s) {
           const int i = kPre + (s < kUnst ? s : s - kUnst);
           if (i < kPairs)
-            bld16_lds(s < kUnst ? nt : nd, &sh_pre[s][1][wbase], coff[i % NV], (i / NV) * p.row_bytes);
+            bld16_lds<kCp>(s < kUnst ? nt : nd, &sh_pre[s][1][wbase], coff[i % NV], (i / NV) * p.row_bytes);
         }
       };
       if constexpr (kAhead) {
@@ -934,15 +939,15 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
 #pragma unroll
         for (int e = 0; e < E; ++e) g[e] = cA * ex2(__builtin_fmaf(xd[e], p.scd, -mscd));
       }
-      store_g<TG, E>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
+      store_g<TG, E, kCp>(gr, uint32_t(col[v]) * uint32_t(E * GS), g);
       asm volatile("" ::: "memory");
       if (i < kPre) {
         rd[k][v] = sh_pre[i][0][tid];
         if (i >= kFree) rt[k][v] = sh_pre[i][1][tid];  // pairs below kFree were refilled after merge A
       } else {
         const int sd = kEarly ? rslot_d(i) : -1, st = kEarly ? rslot_t(i) : -1;
-        rd[k][v] = sd >= 0 ? sh_pre[sd][1][tid] : bld16(nd, coff[v], k * p.row_bytes);
-        rt[k][v] = st >= 0 ? sh_pre[st][1][tid] : bld16(nt, coff[v], k * p.row_bytes);
+        rd[k][v] = sd >= 0 ? sh_pre[sd][1][tid] : bld16<kCp>(nd, coff[v], k * p.row_bytes);
+        rt[k][v] = st >= 0 ? sh_pre[st][1][tid] : bld16<kCp>(nt, coff[v], k * p.row_bytes);
       }
       if constexpr (KLC) {
         // the last pair of row k in this order: (jp + kPre) % kPairs runs
