@@ -140,6 +140,14 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   // a case the fused EAL/WTV kernel serves), nontemporal otherwise.
   constexpr int kCp = kAhead ? 0 : kNontemporal;
   constexpr int KE = kAhead ? K0 : 1;
+  // Greedy-token variants without a phase B: between publishing a chunk's
+  // phase-A partials and polling the team's, each wave takes, for the next
+  // chunk's first (staged) rows, the target maximum over each thread's
+  // columns and the row's greedy token over the wave (value, lowest index,
+  // owning lane), reading the staged target copies from LDS; phase A then
+  // skips that part (the draft payload is read from the owning lane).
+  constexpr int kGA = (AM && !HB) ? (kPre / NV < 4 ? (kPre / NV < K ? kPre / NV : K) : (K < 4 ? K : 4)) : 0;
+  constexpr int kGAR = kGA > 0 ? kGA : 1;
   constexpr int kPairsPerReg = 32 / E;
   constexpr int kMaskRegs = MB ? (kPairs + kPairsPerReg - 1) / kPairsPerReg : 1;
   __shared__ u32x4 sh_pre[kPre][2][kBlock];
@@ -201,6 +209,53 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   auto rslot_t = [](int i) { return (i - kPre) < kFree ? i - kPre : -1; };
   auto rslot_d = [](int i) { return kUnst + (i - kPre) < kFree ? kUnst + (i - kPre) : -1; };
   float em[KE], es[KE];
+  float gmt[kGAR], gbest[kGAR];
+  int gx[kGAR], gsrc[kGAR];
+  // row k's greedy-token look-ahead from the target vectors tv (masked past the row end)
+  auto greedy_ahead = [&](const u32x4 (&tv)[NV], int k) {
+    float xs[NV][E];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) unpackv<TI, E>(tv[v], xs[v]);
+    float mt = kNegInf;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+    int li = 0;
+#pragma unroll
+    for (int v = NV - 1; v >= 0; --v)
+#pragma unroll
+      for (int e = E - 1; e >= 0; --e)
+        if (xs[v][e] == mt) li = v * E + e;
+    const int idx = mt == kNegInf ? INT_MAX : col[0] * E + (li / E) * (kBlock * E) + li % E;
+    float m[1] = {mt};
+    wave_max_n(m);
+    const int x = wave_min_i(mt == m[0] ? idx : INT_MAX);
+    const uint64_t own = __builtin_amdgcn_ballot_w64(mt == m[0] && idx == x);
+    gmt[k] = mt;
+    gbest[k] = m[0];
+    gx[k] = x;
+    gsrc[k] = own != 0 ? __builtin_ctzll(own) : 0;
+  };
+  // the draft logit at element x of row k (wave-uniform x, held by lane src)
+  auto draft_at = [&](int k, int x, int src) {
+    if (x == INT_MAX) return kNegInf;
+    const int c = x / E - member * (kBlock * NV);
+    const int vv = c / kBlock, e = x % E;
+    constexpr int EPW = E / 4;
+    const int q = e / EPW;
+    uint32_t wd = 0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq)
+        if (v == vv && qq == q) wd = __builtin_amdgcn_readlane(rd[k][v][qq], src);
+    if constexpr (EPW == 2) {
+      return __builtin_bit_cast(float, (e & 1) ? (wd & 0xffff0000u) : (wd << 16));
+    } else {
+      return __builtin_bit_cast(float, wd);
+    }
+  };
   // the target's (max, sum-exp) partial of row k over this thread's columns
   auto target_partial = [&](int k, float& mo, float& so) {
     float xs[NV][E];
@@ -274,6 +329,15 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       for (int k = 0; k < K0; ++k) {
         if (last) mask_tail(rt, k);
         target_partial(k, em[k], es[k]);
+      }
+    }
+    if constexpr (kGA > 0) {
+#pragma unroll
+      for (int k = 0; k < kGA; ++k) {
+        u32x4 tv[NV];
+#pragma unroll
+        for (int v = 0; v < NV; ++v) tv[v] = col[v] >= p.ng ? neg_inf_vec(TI{}) : rt[k][v];
+        greedy_ahead(tv, k);
       }
     }
   }
@@ -377,10 +441,14 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
 #pragma unroll
           for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
           float mt = kNegInf;  // the target's maximum (normaliser and greedy token)
+          if (k < kGA) {
+            mt = gmt[k < kGAR ? k : 0];  // taken during the previous chunk's merge
+          } else {
 #pragma unroll
-          for (int v = 0; v < NV; ++v)
+            for (int v = 0; v < NV; ++v)
 #pragma unroll
-            for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+              for (int e = 0; e < E; ++e) mt = fmaxf(mt, xs[v][e]);
+          }
           if constexpr (PQ) {
             const float mtsc = mt * p.sct;
             float st = 0.f;
@@ -397,8 +465,15 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
             s1[k] = st;
           }
           float best = mt, bi, bz;
-          first_max<TI, NV, E, kBlock>(xs, rd[k], mt, col[0] * E, bi, bz);
-          wave_argmax(best, bi, bz);
+          if (k < kGA) {
+            const int kk = k < kGAR ? k : 0;
+            best = gbest[kk];
+            bi = __builtin_bit_cast(float, gx[kk]);
+            bz = draft_at(k, gx[kk], gsrc[kk]);
+          } else {
+            first_max<TI, NV, E, kBlock>(xs, rd[k], mt, col[0] * E, bi, bz);
+            wave_argmax(best, bi, bz);
+          }
           // wave-uniform from here: stored right away rather than kept live
           if (lane == 0) {
             sh_w[wv][k][4] = best;
@@ -698,6 +773,19 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
 
     // ------------------------------------------------------------ phase B
     if constexpr (!HB) {
+      if constexpr (kGA > 0) {
+        wait_vmem_all();  // the next chunk's staging (issued in phase A) has landed
+#pragma unroll
+        for (int k = 0; k < kGA; ++k) {
+          u32x4 tv[NV];
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            tv[v] = sh_pre[k * NV + v][1][tid];
+            if (last && col[v] >= p.ng) tv[v] = neg_inf_vec(TI{});
+          }
+          greedy_ahead(tv, k);
+        }
+      }
       merge_a(0, K);
       if (tid < K) {
         sh_b[tid][0] = 0.f;
