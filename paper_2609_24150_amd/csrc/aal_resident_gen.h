@@ -134,12 +134,17 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   // data), the first group's target partials of a chunk are evaluated during
   // the previous chunk's last team merge, with a first group of 4 rows.
   constexpr bool kAhead = kEarly && !AM && K0 == 4;
+  // With a phase B and no early refill (a KL term with a TV term) the staged
+  // copies stay in LDS until phase C: the first rows' target partials of the
+  // next chunk are then evaluated from them during the last team merge.
+  constexpr int kLtMax = kPre / NV < K0 ? kPre / NV : K0;
+  constexpr int kLT = (PQ && !AM && HB && !kEarly && K0 < K) ? (kLtMax < 4 ? kLtMax : 4) : 0;
   // Cache policy of the logit loads and gradient stores: ordinary cached
   // accesses for the look-ahead variants (sliding WTV over 7 x 2048 rows of
   // V = 128256 0.8% faster than nontemporal ones; disjoint windows 1% slower,
   // a case the fused EAL/WTV kernel serves), nontemporal otherwise.
   constexpr int kCp = kAhead ? 0 : kNontemporal;
-  constexpr int KE = kAhead ? K0 : 1;
+  constexpr int KE = kAhead ? K0 : (kLT > 0 ? kLT : 1);
   // Greedy-token variants without a phase B: between publishing a chunk's
   // phase-A partials and polling the team's, each wave takes, for the next
   // chunk's first (staged) rows, the target maximum over each thread's
@@ -256,11 +261,12 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       return __builtin_bit_cast(float, wd);
     }
   };
-  // the target's (max, sum-exp) partial of row k over this thread's columns
-  auto target_partial = [&](int k, float& mo, float& so) {
+  // the target's (max, sum-exp) partial of a row over this thread's columns
+  // (its vectors tv)
+  auto target_partial_v = [&](const u32x4 (&tv)[NV], float& mo, float& so) {
     float xs[NV][E];
 #pragma unroll
-    for (int v = 0; v < NV; ++v) unpackv<TI, E>(rt[k][v], xs[v]);
+    for (int v = 0; v < NV; ++v) unpackv<TI, E>(tv[v], xs[v]);
     float mt = kNegInf;
 #pragma unroll
     for (int v = 0; v < NV; ++v)
@@ -279,6 +285,21 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
     }
     mo = mt == kNegInf ? kNegInf : mtsc;
     so = st;
+  };
+  auto target_partial = [&](int k, float& mo, float& so) { target_partial_v(rt[k], mo, so); };
+  // kLT: the next chunk's first target partials from the staged copies
+  auto staged_target_ahead = [&]() {
+    wait_vmem_all();  // the next chunk's staging (issued in phase A) has landed
+#pragma unroll
+    for (int k = 0; k < kLT; ++k) {
+      u32x4 tv[NV];
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        tv[v] = sh_pre[k * NV + v][1][tid];
+        if (last && col[v] >= p.ng) tv[v] = neg_inf_vec(TI{});
+      }
+      target_partial_v(tv, em[k], es[k]);
+    }
   };
   auto mask_tail = [&](u32x4 (&r)[K][NV], int k) {
 #pragma unroll
@@ -338,6 +359,15 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
 #pragma unroll
         for (int v = 0; v < NV; ++v) tv[v] = col[v] >= p.ng ? neg_inf_vec(TI{}) : rt[k][v];
         greedy_ahead(tv, k);
+      }
+    }
+    if constexpr (kLT > 0) {
+#pragma unroll
+      for (int k = 0; k < kLT; ++k) {
+        u32x4 tv[NV];
+#pragma unroll
+        for (int v = 0; v < NV; ++v) tv[v] = col[v] >= p.ng ? neg_inf_vec(TI{}) : rt[k][v];
+        target_partial_v(tv, em[k], es[k]);
       }
     }
   }
@@ -430,7 +460,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         m1[k] = kNegInf;
         s1[k] = 0.f;
         if constexpr (PQ && !AM) {
-          if (kAhead && k < K0) {  // evaluated during the previous chunk's last merge
+          if ((kAhead && k < K0) || k < kLT) {  // evaluated during the previous chunk's last merge
             m1[k] = em[k < KE ? k : 0];
             s1[k] = es[k < KE ? k : 0];
           } else {
@@ -847,6 +877,9 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           for (int k = 0; k < K0; ++k) target_partial(k, em[k], es[k]);
         }
       }
+      if constexpr (kLT > 0) {
+        if (p.CS == 1) staged_target_ahead();
+      }
       merge_b(0, K);
     }
     lds_barrier();
@@ -867,6 +900,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
 #pragma unroll
         for (int k = 0; k < K0; ++k) target_partial(k, em[k], es[k]);
       }
+      if constexpr (kLT > 0) staged_target_ahead();
       if (wv == 0 && lane < 2 * K) {
         const int o = lane < K ? lane - K : lane;  // offset from row0: -K..-1, K..2K-1
         const int pos = j * K + o;                 // position in the sequence

@@ -178,7 +178,7 @@ def test_sequences_match_resident_wtv_for_single_window_sequences(A, flags):
     assert d <= 2 * w["grad"].float().abs().max().item() * 2 ** -8
 
 
-@pytest.mark.parametrize("weights", [(1, 0, 0, 0), (0, 0.1, 1, 0), (0.7, 0.4, 1.3, 0.9)])
+@pytest.mark.parametrize("weights", [(1, 0, 0, 0), (0, 0.1, 1, 0), (0, 0, 1, 1), (0.7, 0.4, 1.3, 0.9)])
 def test_many_chunks_and_members(A, weights, flags):
     """Sequences of 150 positions (22 chunks of 7, the last of 3 rows) with a
     vocabulary split over 4 workgroups per chunk, so that chunks outnumber the
