@@ -148,9 +148,10 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   // Greedy-token variants without a phase B: between publishing a chunk's
   // phase-A partials and polling the team's, each wave takes, for the next
   // chunk's first (staged) rows, the target maximum over each thread's
-  // columns and the row's greedy token over the wave (value, lowest index,
-  // owning lane), reading the staged target copies from LDS; phase A then
-  // skips that part (the draft payload is read from the owning lane).
+  // columns (with its sum-exp partial when the target is normalised) and the
+  // row's greedy token over the wave (value, lowest index, owning lane),
+  // reading the staged target copies from LDS; phase A then skips that part
+  // (the draft payload is read from the owning lane).
   constexpr int kGA = (AM && !HB) ? (kPre / NV < 4 ? (kPre / NV < K ? kPre / NV : K) : (K < 4 ? K : 4)) : 0;
   constexpr int kGAR = kGA > 0 ? kGA : 1;
   constexpr int kPairsPerReg = 32 / E;
@@ -214,7 +215,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
   auto rslot_t = [](int i) { return (i - kPre) < kFree ? i - kPre : -1; };
   auto rslot_d = [](int i) { return kUnst + (i - kPre) < kFree ? kUnst + (i - kPre) : -1; };
   float em[KE], es[KE];
-  float gmt[kGAR], gbest[kGAR];
+  float gmt[kGAR], gbest[kGAR], gst[kGAR];
   int gx[kGAR], gsrc[kGAR];
   // row k's greedy-token look-ahead from the target vectors tv (masked past the row end)
   auto greedy_ahead = [&](const u32x4 (&tv)[NV], int k) {
@@ -233,6 +234,20 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
       for (int e = E - 1; e >= 0; --e)
         if (xs[v][e] == mt) li = v * E + e;
     const int idx = mt == kNegInf ? INT_MAX : col[0] * E + (li / E) * (kBlock * E) + li % E;
+    if constexpr (PQ) {  // the sum-exp partial that phase A pairs with this maximum
+      const float mtsc = mt * p.sct;
+      float st = 0.f;
+      if (mt != kNegInf) {
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const float xe = ex2(__builtin_fmaf(xs[v][e], p.sct, -mtsc));
+            st = (v == 0 && e == 0) ? xe : st + xe;
+          }
+      }
+      gst[k] = st;
+    }
     float m[1] = {mt};
     wave_max_n(m);
     const int x = wave_min_i(mt == m[0] ? idx : INT_MAX);
@@ -482,7 +497,9 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
           if constexpr (PQ) {
             const float mtsc = mt * p.sct;
             float st = 0.f;
-            if (mt != kNegInf) {
+            if (k < kGA) {
+              st = gst[k < kGAR ? k : 0];
+            } else if (mt != kNegInf) {
 #pragma unroll
               for (int v = 0; v < NV; ++v)
 #pragma unroll
