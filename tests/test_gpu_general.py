@@ -187,6 +187,15 @@ def test_many_chunks_and_members(A, weights, flags):
     _check(A, zd, zt, 7, weights, SEQ, flags=flags)
 
 
+@pytest.mark.parametrize("weights", [(0, 0.1, 1, 0), (0, 0, 1, 1)])
+def test_many_chunks_ragged_last_member(A, weights):
+    """As above with V = 32000: the team's last workgroup holds 928 of its 1024
+    vectors, so the rows evaluated ahead from the staged copies are masked past
+    the row end as the rows in registers are."""
+    zd, zt = _inputs(3, 150, 32000, torch.bfloat16, seed=33)
+    _check(A, zd, zt, 7, weights, SEQ)
+
+
 @pytest.mark.parametrize("weights", [(0, 0, 1, 0), (0, 0.1, 1, 0), (0, 0.1, 1, 0.5), (0.5, 0, 1, 0)])
 @pytest.mark.parametrize("layout,shape", [(WIN, (6, 5, 4096)), (SEQ, (2, 33, 4096))])
 def test_without_per_row_outputs(A, weights, layout, shape, flags):
