@@ -196,6 +196,33 @@ def test_many_chunks_ragged_last_member(A, weights):
     _check(A, zd, zt, 7, weights, SEQ)
 
 
+def test_greedy_ties_across_members_many_windows(A, flags):
+    """KL + 0.1 EAL over 40 windows of 7 rows at V = 128256 (16-member teams,
+    so windows 16-39 are a team's second or third window) with tied greedy
+    maxima in different members, in rows whose token is taken ahead during
+    the previous window's merge (rows 0-3) and in rows taken in phase A: the
+    lowest index wins, and a_eal = q(x*) matches the oracle."""
+    N, K, V = 40, 7, 128256
+    g = torch.Generator(device="cpu").manual_seed(35)
+    zt = torch.randn(N, K, V, generator=g) * 2.5
+    zd = 0.7 * zt + torch.randn(N, K, V, generator=g) * 1.5
+    ties = [(0, 0, [100, 125000]), (17, 1, [8191, 8192]), (17, 5, [64, 512, 128000]),
+            (33, 3, [24576, 127000, 3]), (39, 2, list(range(0, V, 8192))), (20, 6, [125000, 128255])]
+    for n, k, cols in ties:
+        zt[n, k, cols] = 40.0
+    a, b = zd.to(torch.bfloat16).cuda(), zt.to(torch.bfloat16).cuda()
+    r = A.aal_loss_fwd_bwd(a, b, K, weights=(0, 0.1, 1, 0), layout=WIN, flags=flags)
+    torch.cuda.synchronize()
+    xs = r["xstar"].cpu().numpy().reshape(N, K)
+    for n, k, cols in ties:
+        assert xs[n, k] == min(cols), (n, k, xs[n, k])
+    zd64, zt64 = host64(a), host64(b)
+    assert np.array_equal(xs, O.greedy_token(zt64))
+    a_o, _, _ = O.acceptance_greedy(zd64, zt64, 1.0)
+    np.testing.assert_allclose(host64(r["accept_eal"]).reshape(N, K), a_o,
+                               rtol=1e-3, atol=1e-7)
+
+
 @pytest.mark.parametrize("weights", [(0, 0, 1, 0), (0, 0.1, 1, 0), (0, 0.1, 1, 0.5), (0.5, 0, 1, 0)])
 @pytest.mark.parametrize("layout,shape", [(WIN, (6, 5, 4096)), (SEQ, (2, 33, 4096))])
 def test_without_per_row_outputs(A, weights, layout, shape, flags):
