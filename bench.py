@@ -544,6 +544,7 @@ def main():
             # the same rows read as 7 sequences of 2048 positions, windows sliding by one
             legs = [("wtv_sliding_7x2048", _lib.AAL_LAYOUT_SEQUENCES, 7, 2048, (1.0, 0.0, 0.0, 0.0)),
                     ("kl_plus_0.1eal_c2", _lib.AAL_LAYOUT_WINDOWS, N, K, (0.0, 0.1, 1.0, 0.0)),
+                    ("kl_plus_0.1eal_sliding_7x2048", _lib.AAL_LAYOUT_SEQUENCES, 7, 2048, (0.0, 0.1, 1.0, 0.0)),
                     ("kl_plus_tv_c2", _lib.AAL_LAYOUT_WINDOWS, N, K, (0.0, 0.0, 1.0, 1.0))]
             for name, layout, B_, S_, wts in legs:
                 fn_g, st_g, R_, W_, o_g = general_call(zd, zt, layout, B_, S_, K, wts, gdt)

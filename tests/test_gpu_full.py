@@ -165,6 +165,48 @@ def test_c2_rows_as_sliding_sequences(A, pool, c2):
     del r
 
 
+def test_c2_rows_as_sliding_sequences_kl_eal(A, pool, c2):
+    """KL + 0.1 EAL (the paper's greedy recipe) over the c2 rows as 7 sequences
+    of 2048 positions with windows sliding by one: every row's greedy token,
+    a_eal and KL, every window's E and the loss against the oracle, and the
+    gradient of every row against the oracle on the sub-sequence that holds
+    every window containing it."""
+    d, sh, specs = c2
+    zd, zt = d["z_draft"], d["z_target"]
+    N, K, V = zd.shape
+    B, S = 7, N * K // 7
+    R, W = B * S, B * (S - K + 1)
+    w = (0.0, 0.1, 1.0, 0.0)
+    r = A.aal_loss_fwd_bwd(zd.view(B, S, V), zt.view(B, S, V), K, weights=w, layout=A.AAL_LAYOUT_SEQUENCES)
+    torch.cuda.synchronize()
+    gspec = sh.put(r["grad"].view(R, V))
+    rspecs = {"zd": (specs["zd"][0], (R, V), specs["zd"][2]), "zt": (specs["zt"][0], (R, V), specs["zt"][2]),
+              "grad": gspec}
+    res = FC.run(pool, "seqgrad", rspecs, R, 64, {"S": S, "K": K, "w": w, "Td": 1.0, "Tt": 1.0, "R": R, "W": W})
+    sh.drop(gspec)
+    # per-row greedy token, acceptance and KL from the oracle, then the sliding windows
+    res_a = FC.run(pool, "combined", {"zd": rspecs["zd"], "zt": rspecs["zt"]}, R, 56,
+                   {"K": 1, "Td": 1.0, "Tt": 1.0, "w": w, "N": R})
+    a_o, kl_o = FC.cat(res_a, "a_eal").reshape(-1), FC.cat(res_a, "kl").reshape(-1)
+    assert np.array_equal(r["xstar"].cpu().numpy().reshape(-1), FC.cat(res_a, "xstar").reshape(-1))
+    E_o, _ = O.window_length_coefficients(a_o, O.window_rows(O.LAYOUT_SEQUENCES, B, S, K))
+    tol = loss_tol(zd.dtype)
+    assert rel_err(host64(r["E_eal"]), E_o) <= tol
+    np.testing.assert_allclose(host64(r["accept_eal"]), a_o, rtol=tol, atol=1e-4)
+    terms_o = np.array([0.0, -np.mean(E_o), np.mean(kl_o), 0.0])
+    terms = host64(r["terms"])
+    for t in (1, 2):
+        assert rel_err(terms[t], terms_o[t]) <= tol, (t, terms[t], terms_o[t])
+    loss_o = float(np.dot(w, terms_o))
+    assert rel_err(r["loss"].item(), loss_o) <= tol
+    g = FC.merge_grad(res)
+    _check_grad_totals("c2_sliding_kl_eal", g, R)
+    FC.report("c2_rows_sliding_kl_plus_0.1eal_7x2048", {"windows": W, "rows": R, "loss": r["loss"].item(),
+                                                        "loss_oracle": loss_o, "terms": terms.tolist(),
+                                                        "terms_oracle": terms_o.tolist(), "grad": g})
+    del r
+
+
 @pytest.mark.parametrize("w,name", [((0.0, 0.1, 1.0, 0.0), "kl_plus_0.1eal"), ((0.0, 0.0, 1.0, 1.0), "kl_plus_tv")])
 def test_c2_combined_objectives_full(A, pool, c2, w, name):
     """KL + 0.1 EAL (the paper's greedy recipe) and KL + TV over the c2 windows:
