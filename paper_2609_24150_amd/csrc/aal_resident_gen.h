@@ -823,19 +823,25 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
     if constexpr (K0 < K) phase_a(IK0{}, IK{});
 
     // ------------------------------------------------------------ phase B
-    if constexpr (!HB) {
-      if constexpr (kGA > 0) {
-        wait_vmem_all();  // the next chunk's staging (issued in phase A) has landed
+    // kGA: the next chunk's greedy tokens from the staged target copies
+    auto staged_greedy_ahead = [&]() {
+      wait_vmem_all();  // the next chunk's staging (issued in phase A) has landed
 #pragma unroll
-        for (int k = 0; k < kGA; ++k) {
-          u32x4 tv[NV];
+      for (int k = 0; k < kGA; ++k) {
+        u32x4 tv[NV];
 #pragma unroll
-          for (int v = 0; v < NV; ++v) {
-            tv[v] = sh_pre[k * NV + v][1][tid];
-            if (last && col[v] >= p.ng) tv[v] = neg_inf_vec(TI{});
-          }
-          greedy_ahead(tv, k);
+        for (int v = 0; v < NV; ++v) {
+          tv[v] = sh_pre[k * NV + v][1][tid];
+          if (last && col[v] >= p.ng) tv[v] = neg_inf_vec(TI{});
         }
+        greedy_ahead(tv, k);
+      }
+    };
+    if constexpr (!HB) {
+      // before the merge for disjoint windows; for sliding ones in the
+      // neighbour exchange below, off the ring of neighbour dependencies
+      if constexpr (kGA > 0) {
+        if (p.CS == 1) staged_greedy_ahead();
       }
       merge_a(0, K);
       if (tid < K) {
@@ -922,6 +928,7 @@ __global__ __launch_bounds__(kGenBlock) void k_res_gen(GenResParams p) {
         for (int k = 0; k < K0; ++k) target_partial(k, em[k], es[k]);
       }
       if constexpr (kLT > 0) staged_target_ahead();
+      if constexpr (kGA > 0) staged_greedy_ahead();
       if (wv == 0 && lane < 2 * K) {
         const int o = lane < K ? lane - K : lane;  // offset from row0: -K..-1, K..2K-1
         const int pos = j * K + o;                 // position in the sequence
